@@ -1,0 +1,143 @@
+/*
+ * sched_search.h -- brute-force device-mapping search on one AMD Instinct MI355X.
+ *
+ * A workflow is a DAG of tools; every tool runs in one of three modes
+ * (Section 2.1): 0 = cpu, 1 = gpu_now (immediate GPU, holds its footprint
+ * while it runs, an over-budget start is an out-of-memory failure), 2 =
+ * gpu_queue (serialized GPU queue, holds no VRAM while waiting, pays load-in).
+ * A mapping assigns a mode to every tool; its index is sum_v mode_v * 3^v
+ * (tool 0 is the least significant digit).  The library scores mappings with
+ * an integer event-driven schedule (GPU-utilisation contention as a Q16
+ * slowdown fixed at each GPU start by the number of co-running GPU tools,
+ * VRAM admission, FIFO queue on (ready time, tool), PCIe transfer charged to
+ * the consumer of an edge whose ends sit on different devices) and returns
+ * the feasible mapping of lowest makespan, ties to the lowest index: the
+ * exhaustive-search reference of Sections 2.3 and 4.1, with the measured
+ * latency replaced by the model.
+ *
+ * Units: time in integer microseconds, memory in integer MiB, contention
+ * factors in Q16 (65536 = 1.0x).  All calls are thread-safe on distinct
+ * workspaces; a problem handle is immutable after creation.
+ *
+ * Ownership: every host pointer argument is owned by the caller and only
+ * read (or, for outputs, written) during the call.  The library never
+ * allocates device memory: device work runs in the caller's workspace on the
+ * caller's HIP stream, and every entry point that launches work waits for
+ * that stream before returning.  On error no output is written.
+ */
+#ifndef SCHED_SEARCH_H
+#define SCHED_SEARCH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Error codes (negative; 0 is success). */
+#define SCHED_OK 0
+#define SCHED_E_NULL (-1)      /* a required pointer is null */
+#define SCHED_E_SIZE (-2)      /* n_tools not in [1,40], n_levels not in [1,64],
+                                  a negative count, n_replicas < 1 */
+#define SCHED_E_VALUE (-3)     /* gpu_us or cpu_us < 1; load, xfer, mem or
+                                  budget < 0; a factor < 65536 or > 2^24 */
+#define SCHED_E_EDGE (-4)      /* edge endpoint out of range, or a self-loop */
+#define SCHED_E_CYCLE (-5)     /* the edges contain a cycle */
+#define SCHED_E_RANGE (-6)     /* lo >= hi or hi > 3^N; replica map out of range */
+#define SCHED_E_OVERFLOW (-7)  /* the worst-case makespan bound reaches 2^31 us,
+                                  or (N+1)*(budget+1) reaches 2^32: the device
+                                  path keeps times and VRAM sums in 32 bits */
+#define SCHED_E_WORKSPACE (-8) /* workspace null, misaligned (256 B) or too small */
+#define SCHED_E_DEVICE (-9)    /* a HIP runtime call failed */
+#define SCHED_E_NOMEM (-10)    /* host allocation failed */
+
+/* Tool card: the per-tool profile of Section 3.1 (CPU, GPU and load-in times,
+ * VRAM footprint) plus the input-transfer cost paid when a predecessor runs
+ * on the other device. */
+typedef struct {
+    int64_t gpu_us;  /* isolated GPU latency, >= 1 */
+    int64_t cpu_us;  /* isolated CPU latency, >= 1 */
+    int64_t load_us; /* load-in paid by gpu_queue, >= 0 */
+    int64_t xfer_us; /* input transfer across devices, >= 0 */
+    int64_t mem_mib; /* VRAM footprint while running on the GPU, >= 0 */
+} sched_tool;
+
+/* Re-measured latencies of one replica (running averages, Section 3.2);
+ * footprints, edges, budget and contention stay those of its problem. */
+typedef struct {
+    int64_t gpu_us, cpu_us, load_us, xfer_us;
+} sched_lat;
+
+/* Data dependency: dst starts only after src completes (Section 2.1). */
+typedef struct {
+    int32_t src, dst;
+} sched_edge;
+
+/* Search result.  With no feasible mapping in the range: best_index =
+ * UINT64_MAX and makespan_us = INT64_MAX (on a full range this cannot
+ * happen: index 0, all tools on the CPU, is always feasible). */
+typedef struct {
+    uint64_t best_index;
+    int64_t makespan_us;
+} sched_result;
+
+typedef struct sched_problem sched_problem;
+
+/* Validate and freeze a problem (Section 2.1: DAG G=(V,E), modes, tau,
+ * budget M).  tools: n_tools cards; edges: n_edges pairs (duplicates are
+ * ignored); contention_q16: F[k-1] for k = 1..n_levels co-running GPU tools,
+ * each in [65536, 2^24], levels beyond n_levels use the last one;
+ * vram_budget_mib: the budget M.  On success *out receives a handle to free
+ * with sched_problem_destroy.  Host-only: touches no device. */
+int sched_problem_create(const sched_tool *tools, int32_t n_tools,
+                         const sched_edge *edges, int32_t n_edges,
+                         const uint32_t *contention_q16, int32_t n_levels,
+                         int64_t vram_budget_mib, sched_problem **out);
+
+void sched_problem_destroy(sched_problem *p);
+
+/* Number of tools and of mappings (3^N) of a problem. */
+int sched_num_tools(const sched_problem *p, int32_t *out);
+int sched_num_mappings(const sched_problem *p, uint64_t *out);
+
+/* Bytes of device workspace sufficient for any call below on these
+ * problems with up to n_replicas replicas (n_replicas = 0 for calls without
+ * replicas).  Host-only. */
+int sched_workspace_bytes(const sched_problem *const *problems, int32_t n_problems,
+                          int32_t n_replicas, size_t *out);
+
+/* Exhaustive search over mapping indices [lo, hi) of problem p (the oracle
+ * of Sections 2.3 and 4.1).  d_workspace: device memory of ws_bytes, 256-byte
+ * aligned; hip_stream: a hipStream_t (null = default stream).  Writes *h_out
+ * (host) after the stream has finished. */
+int sched_bruteforce_argmin(const sched_problem *p, uint64_t lo, uint64_t hi,
+                            void *d_workspace, size_t ws_bytes, void *hip_stream,
+                            sched_result *h_out);
+
+/* Batched re-scoring of perturbed profiles (the running-average feedback of
+ * Section 3.2): replica r is problem replica_problem[r] with the latencies
+ * replica_lat[off_r .. off_r + N_r), where off_r is the sum of N over the
+ * earlier replicas.  Each replica gets its own exhaustive search over all
+ * 3^N mappings; h_out[r] receives its result. */
+int sched_eval_batch(const sched_problem *const *problems, int32_t n_problems,
+                     const int32_t *replica_problem, const sched_lat *replica_lat,
+                     int32_t n_replicas, void *d_workspace, size_t ws_bytes,
+                     void *hip_stream, sched_result *h_out);
+
+/* Score explicit mappings (the what-if probes of Section 3.2): d_idx and
+ * d_makespan are device arrays of n entries; each index must be < 3^N.
+ * d_makespan[i] receives the makespan of d_idx[i] in us, or INT64_MAX when
+ * that mapping is infeasible.  Out-of-range indices also yield INT64_MAX. */
+int sched_eval_mappings(const sched_problem *p, const uint64_t *d_idx, int64_t n,
+                        int64_t *d_makespan, void *d_workspace, size_t ws_bytes,
+                        void *hip_stream);
+
+/* Static text for an error code. */
+const char *sched_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCHED_SEARCH_H */

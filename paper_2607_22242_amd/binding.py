@@ -1,0 +1,225 @@
+"""ctypes binding of libsched.so (include/sched_search.h), same names.
+
+Argument marshalling only: every step of the search runs in the HIP
+library.  PyTorch supplies device memory (the workspace, index and output
+tensors) and the HIP stream.  If libsched.so has not been built, every call
+raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsched.so")
+
+SCHED_OK = 0
+ERRORS = {
+    -1: "SCHED_E_NULL", -2: "SCHED_E_SIZE", -3: "SCHED_E_VALUE", -4: "SCHED_E_EDGE",
+    -5: "SCHED_E_CYCLE", -6: "SCHED_E_RANGE", -7: "SCHED_E_OVERFLOW",
+    -8: "SCHED_E_WORKSPACE", -9: "SCHED_E_DEVICE", -10: "SCHED_E_NOMEM",
+}
+NO_INDEX = (1 << 64) - 1
+INFEASIBLE = (1 << 63) - 1
+
+EXPORTED = ["sched_problem_create", "sched_problem_destroy", "sched_num_tools",
+            "sched_num_mappings", "sched_workspace_bytes", "sched_bruteforce_argmin",
+            "sched_eval_batch", "sched_eval_mappings", "sched_strerror"]
+
+
+class sched_tool(ctypes.Structure):
+    _fields_ = [("gpu_us", ctypes.c_int64), ("cpu_us", ctypes.c_int64),
+                ("load_us", ctypes.c_int64), ("xfer_us", ctypes.c_int64),
+                ("mem_mib", ctypes.c_int64)]
+
+
+class sched_lat(ctypes.Structure):
+    _fields_ = [("gpu_us", ctypes.c_int64), ("cpu_us", ctypes.c_int64),
+                ("load_us", ctypes.c_int64), ("xfer_us", ctypes.c_int64)]
+
+
+class sched_edge(ctypes.Structure):
+    _fields_ = [("src", ctypes.c_int32), ("dst", ctypes.c_int32)]
+
+
+class sched_result(ctypes.Structure):
+    _fields_ = [("best_index", ctypes.c_uint64), ("makespan_us", ctypes.c_int64)]
+
+
+class SchedError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        self.name = ERRORS.get(code, str(code))
+        super().__init__(f"{where}: {self.name} ({sched_strerror(code)})")
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libsched.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2607_22242_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        L.sched_problem_create.restype = ctypes.c_int
+        L.sched_problem_create.argtypes = [P, ctypes.c_int32, P, ctypes.c_int32, P,
+                                           ctypes.c_int32, ctypes.c_int64,
+                                           ctypes.POINTER(ctypes.c_void_p)]
+        L.sched_problem_destroy.restype = None
+        L.sched_problem_destroy.argtypes = [P]
+        L.sched_num_tools.restype = ctypes.c_int
+        L.sched_num_tools.argtypes = [P, ctypes.POINTER(ctypes.c_int32)]
+        L.sched_num_mappings.restype = ctypes.c_int
+        L.sched_num_mappings.argtypes = [P, ctypes.POINTER(ctypes.c_uint64)]
+        L.sched_workspace_bytes.restype = ctypes.c_int
+        L.sched_workspace_bytes.argtypes = [P, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.POINTER(ctypes.c_size_t)]
+        L.sched_bruteforce_argmin.restype = ctypes.c_int
+        L.sched_bruteforce_argmin.argtypes = [P, ctypes.c_uint64, ctypes.c_uint64, P,
+                                              ctypes.c_size_t, P, ctypes.POINTER(sched_result)]
+        L.sched_eval_batch.restype = ctypes.c_int
+        L.sched_eval_batch.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32, P,
+                                       ctypes.c_size_t, P, P]
+        L.sched_eval_mappings.restype = ctypes.c_int
+        L.sched_eval_mappings.argtypes = [P, P, ctypes.c_int64, P, P, ctypes.c_size_t, P]
+        L.sched_strerror.restype = ctypes.c_char_p
+        L.sched_strerror.argtypes = [ctypes.c_int]
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, where: str):
+    if rc != SCHED_OK:
+        raise SchedError(rc, where)
+
+
+def sched_strerror(code: int) -> str:
+    return lib().sched_strerror(code).decode()
+
+
+def sched_problem_create(tools: Sequence[Sequence[int]], edges: Sequence[Sequence[int]],
+                         contention_q16: Sequence[int], vram_budget_mib: int):
+    """Handle (ctypes.c_void_p) of a new problem; tool rows are
+    (gpu_us, cpu_us, load_us, xfer_us, mem_mib)."""
+    n = len(tools)
+    t = (sched_tool * max(n, 1))(*[sched_tool(*map(int, row)) for row in tools])
+    e = (sched_edge * max(len(edges), 1))(*[sched_edge(int(u), int(v)) for u, v in edges])
+    f = (ctypes.c_uint32 * max(len(contention_q16), 1))(*map(int, contention_q16))
+    h = ctypes.c_void_p()
+    rc = lib().sched_problem_create(t, n, e if len(edges) else None, len(edges), f,
+                                    len(contention_q16), int(vram_budget_mib), ctypes.byref(h))
+    _check(rc, "sched_problem_create")
+    return h
+
+
+def sched_problem_destroy(handle) -> None:
+    lib().sched_problem_destroy(handle)
+
+
+def sched_num_tools(handle) -> int:
+    out = ctypes.c_int32()
+    _check(lib().sched_num_tools(handle, ctypes.byref(out)), "sched_num_tools")
+    return out.value
+
+
+def sched_num_mappings(handle) -> int:
+    out = ctypes.c_uint64()
+    _check(lib().sched_num_mappings(handle, ctypes.byref(out)), "sched_num_mappings")
+    return out.value
+
+
+def _handles(handles) -> ctypes.Array:
+    return (ctypes.c_void_p * len(handles))(*[h.value for h in handles])
+
+
+def sched_workspace_bytes(handles: Sequence, n_replicas: int = 0) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().sched_workspace_bytes(_handles(handles), len(handles), n_replicas,
+                                       ctypes.byref(out)), "sched_workspace_bytes")
+    return out.value
+
+
+def _stream_ptr(stream) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _ws(workspace) -> Tuple[int, int]:
+    return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
+def sched_bruteforce_argmin(handle, lo: int, hi: int, workspace, stream=None) -> Tuple[int, int]:
+    """(best_index, makespan_us) over mapping indices [lo, hi)."""
+    out = sched_result()
+    wp, wb = _ws(workspace)
+    _check(lib().sched_bruteforce_argmin(handle, lo, hi, wp, wb, _stream_ptr(stream),
+                                         ctypes.byref(out)), "sched_bruteforce_argmin")
+    return out.best_index, out.makespan_us
+
+
+def sched_eval_batch(handles: Sequence, replica_problem: Sequence[int],
+                     replica_lat: Sequence[Sequence[Sequence[int]]], workspace,
+                     stream=None) -> List[Tuple[int, int]]:
+    """Per-replica (best_index, makespan_us); replica_lat[r] holds N rows of
+    (gpu_us, cpu_us, load_us, xfer_us)."""
+    R = len(replica_problem)
+    rp = (ctypes.c_int32 * max(R, 1))(*map(int, replica_problem))
+    rows = [row for rep in replica_lat for row in rep]
+    lat = (sched_lat * max(len(rows), 1))(*[sched_lat(*map(int, r[:4])) for r in rows])
+    out = (sched_result * max(R, 1))()
+    wp, wb = _ws(workspace)
+    _check(lib().sched_eval_batch(_handles(handles), len(handles), rp, lat, R, wp, wb,
+                                  _stream_ptr(stream), out), "sched_eval_batch")
+    return [(out[i].best_index, out[i].makespan_us) for i in range(R)]
+
+
+def sched_eval_mappings(handle, d_idx, d_makespan, workspace, stream=None) -> None:
+    """Score the device indices d_idx (int64 or uint64 tensor) into the
+    int64 device tensor d_makespan (INT64_MAX = infeasible)."""
+    n = d_idx.numel()
+    assert d_makespan.numel() == n and d_idx.element_size() == 8
+    assert d_idx.is_contiguous() and d_makespan.is_contiguous()
+    wp, wb = _ws(workspace)
+    _check(lib().sched_eval_mappings(handle, d_idx.data_ptr(), n, d_makespan.data_ptr(), wp, wb,
+                                     _stream_ptr(stream)), "sched_eval_mappings")
+
+
+# ---------------------------------------------------------------------------
+# Convenience owner of a handle (marshalling only).
+
+
+class Problem:
+    def __init__(self, tools, edges, contention_q16, vram_budget_mib):
+        self.handle = sched_problem_create(tools, edges, contention_q16, vram_budget_mib)
+        self.n = sched_num_tools(self.handle)
+        self.n_mappings = sched_num_mappings(self.handle)
+
+    @classmethod
+    def from_instance(cls, inst):
+        return cls(inst["tools"], inst["edges"], inst["contention_q16"], inst["vram_budget_mib"])
+
+    def close(self):
+        if self.handle is not None:
+            sched_problem_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def workspace(handles: Sequence, n_replicas: int = 0, device=None):
+    """A 256-byte aligned device workspace tensor large enough for any call."""
+    import torch
+    nbytes = sched_workspace_bytes(handles, n_replicas)
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device or "cuda")
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + nbytes]

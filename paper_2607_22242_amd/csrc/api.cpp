@@ -1,0 +1,434 @@
+// api.cpp -- the C ABI of include/sched_search.h: validation, topological checks,
+// device problem tables, work planning, launches and result copies.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <numeric>
+#include <vector>
+
+#include "sched_search.h"
+#include "devtab.h"
+#include "launch.h"
+
+using namespace devmap;
+
+struct sched_problem {
+  int32_t n = 0;
+  std::vector<sched_tool> tools;
+  std::vector<std::vector<int32_t>> preds;  // ascending, deduplicated
+  std::vector<uint32_t> contention;         // F[k-1]
+  int64_t budget = 0;
+  uint64_t n_mappings = 0;
+  int32_t n_preds = 0;
+  uint32_t table_words = 0;
+  std::vector<uint32_t> table;  // device image with the problem's own latencies
+};
+
+namespace {
+
+constexpr uint32_t kMaxBlocks = 65536;       // cap on search blocks per call
+constexpr uint64_t kTargetLanes = 1ull << 19;  // lanes that fill an MI355X
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+uint64_t pow3(int n) {
+  uint64_t m = 1;
+  for (int i = 0; i < n; ++i) m *= 3u;
+  return m;
+}
+
+// round(b * f / 2^16), halves up, in 128-bit arithmetic.
+uint64_t scale_q16(uint64_t b, uint32_t f) {
+  unsigned __int128 p = (unsigned __int128)b * f + 32768u;
+  unsigned __int128 r = p >> 16;
+  return r > ~0ull ? ~0ull : uint64_t(r);
+}
+
+int check_latencies(int64_t gpu, int64_t cpu, int64_t load, int64_t xfer) {
+  if (gpu < 1 || cpu < 1 || load < 0 || xfer < 0) return SCHED_E_VALUE;
+  return SCHED_OK;
+}
+
+// Fill the device table of problem p with latencies lat (nullptr: the
+// problem's own).  Returns SCHED_E_OVERFLOW when the 32-bit guards fail.
+int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
+  const int n = p.n;
+  const int levels = std::min<int>(int(p.contention.size()), n);
+  std::memset(out, 0, sizeof(uint32_t) * p.table_words);
+
+  int64_t sum_mem = 0;
+  for (const auto& t : p.tools) sum_mem += t.mem_mib;
+  const int64_t budget = std::min<int64_t>(p.budget, sum_mem);
+  // VRAM sums of up to N footprints (each clamped to budget+1) plus the
+  // budget must stay below 2^32.
+  if ((unsigned __int128)(n + 1) * (unsigned __int128)(budget + 1) >= ((unsigned __int128)1 << 32))
+    return SCHED_E_OVERFLOW;
+
+  uint64_t big = 0, src = 0;
+  unsigned __int128 bound = 0;  // worst-case makespan: sum of longest durations + transfers
+  const uint32_t dur_off = kPredBase + ((uint32_t(p.n_preds) + 3u) & ~3u);
+  uint32_t pred_cursor = 0;
+  for (int v = 0; v < n; ++v) {
+    const sched_tool& tl = p.tools[v];
+    const int64_t gpu = lat ? lat[v].gpu_us : tl.gpu_us;
+    const int64_t cpu = lat ? lat[v].cpu_us : tl.cpu_us;
+    const int64_t load = lat ? lat[v].load_us : tl.load_us;
+    const int64_t xfer = lat ? lat[v].xfer_us : tl.xfer_us;
+    if (check_latencies(gpu, cpu, load, xfer) != SCHED_OK) return SCHED_E_VALUE;
+
+    uint64_t longest = uint64_t(cpu);
+    for (int q = 0; q < 2; ++q) {
+      const uint64_t base = q == 0 ? uint64_t(gpu) : uint64_t(gpu) + uint64_t(load);
+      for (int l = 0; l < levels; ++l) {
+        const uint64_t d = scale_q16(base, p.contention[l]);
+        longest = std::max(longest, d);
+        if (d < (1ull << 31)) out[dur_off + (uint32_t(v) * 2u + uint32_t(q)) * uint32_t(levels) + l] = uint32_t(d);
+      }
+    }
+    bound += (unsigned __int128)longest + (unsigned __int128)uint64_t(xfer);
+    if (bound >= ((unsigned __int128)1 << 31)) return SCHED_E_OVERFLOW;
+
+    uint32_t* rec = out + kHdrWords + kToolWords * uint32_t(v);
+    rec[kToolCpu] = uint32_t(cpu);
+    rec[kToolMem] = uint32_t(std::min<int64_t>(tl.mem_mib, budget + 1));
+    rec[kToolXfer] = uint32_t(xfer);
+    uint64_t pm = 0;
+    for (int32_t u : p.preds[v]) pm |= 1ull << u;
+    rec[kToolPredLo] = uint32_t(pm);
+    rec[kToolPredHi] = uint32_t(pm >> 32);
+    rec[kToolPredOff] = pred_cursor;
+    rec[kToolNPred] = uint32_t(p.preds[v].size());
+    for (int32_t u : p.preds[v]) out[kPredBase + pred_cursor++] = uint32_t(u);
+    if (tl.mem_mib > budget) big |= 1ull << v;
+    if (p.preds[v].empty()) src |= 1ull << v;
+  }
+  out[kHdrN] = uint32_t(n);
+  out[kHdrLevels] = uint32_t(levels);
+  out[kHdrBudget] = uint32_t(budget);
+  out[kHdrBigLo] = uint32_t(big);
+  out[kHdrBigHi] = uint32_t(big >> 32);
+  out[kHdrSrcLo] = uint32_t(src);
+  out[kHdrSrcHi] = uint32_t(src >> 32);
+  out[kHdrDurOff] = dur_off;
+  return SCHED_OK;
+}
+
+// Split [lo, hi) x n_tables into blocks of kBlock lanes; each lane owns one
+// outer combination and enumerates 3^J inner ones.
+void plan_search(int n, uint64_t lo, uint64_t hi, uint32_t n_tables, SearchArgs& a) {
+  const uint64_t span = hi - lo;
+  const unsigned __int128 work = (unsigned __int128)span * n_tables;
+  int J = 0;
+  uint64_t inner = 1;
+  while (J < kMaxInnerDigits && J < n && (unsigned __int128)inner * 3u * kTargetLanes <= work) {
+    ++J;
+    inner *= 3u;
+  }
+  a.lo = lo;
+  a.hi = hi;
+  a.inner_digits = uint32_t(J);
+  a.inner_count = uint32_t(inner);
+  a.outer_lo = lo / inner;
+  const uint64_t outer_hi = hi / inner + (hi % inner ? 1 : 0);
+  a.n_outer = outer_hi - a.outer_lo;
+  a.items_per_table = (a.n_outer + kBlock - 1) / kBlock;
+  const uint64_t cap = std::max<uint64_t>(1, kMaxBlocks / n_tables);
+  a.blocks_per_table = uint32_t(std::min<uint64_t>(a.items_per_table, cap));
+  a.n_tables = n_tables;
+}
+
+size_t partial_capacity(uint64_t n_tables) {
+  return size_t(std::max<uint64_t>(n_tables, kMaxBlocks));
+}
+
+struct Layout {
+  size_t tables, partials, results, total;
+};
+
+Layout layout_for(size_t table_bytes_total, size_t n_partials, size_t n_results) {
+  Layout l;
+  l.tables = 0;
+  l.partials = align_up(table_bytes_total);
+  l.results = l.partials + align_up(n_partials * sizeof(Partial));
+  l.total = l.results + align_up(n_results * sizeof(DevResult));
+  return l;
+}
+
+int check_workspace(void* ws, size_t ws_bytes, size_t need) {
+  if (ws == nullptr) return SCHED_E_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0) return SCHED_E_WORKSPACE;
+  if (ws_bytes < need) return SCHED_E_WORKSPACE;
+  return SCHED_OK;
+}
+
+#define HIP_TRY(expr)                                  \
+  do {                                                 \
+    if ((expr) != hipSuccess) return SCHED_E_DEVICE;   \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_edge* edges,
+                         int32_t n_edges, const uint32_t* contention_q16, int32_t n_levels,
+                         int64_t vram_budget_mib, sched_problem** out) {
+  if (out == nullptr || tools == nullptr || contention_q16 == nullptr) return SCHED_E_NULL;
+  if (n_edges > 0 && edges == nullptr) return SCHED_E_NULL;
+  if (n_tools < 1 || n_tools > kMaxTools || n_edges < 0 || n_levels < 1 || n_levels > kMaxLevels)
+    return SCHED_E_SIZE;
+  if (vram_budget_mib < 0) return SCHED_E_VALUE;
+  for (int32_t v = 0; v < n_tools; ++v) {
+    const sched_tool& t = tools[v];
+    if (check_latencies(t.gpu_us, t.cpu_us, t.load_us, t.xfer_us) != SCHED_OK || t.mem_mib < 0)
+      return SCHED_E_VALUE;
+  }
+  for (int32_t l = 0; l < n_levels; ++l)
+    if (contention_q16[l] < 65536u || contention_q16[l] > (1u << 24)) return SCHED_E_VALUE;
+
+  sched_problem* p = new (std::nothrow) sched_problem;
+  if (p == nullptr) return SCHED_E_NOMEM;
+  try {
+    p->n = n_tools;
+    p->tools.assign(tools, tools + n_tools);
+    p->contention.assign(contention_q16, contention_q16 + n_levels);
+    p->budget = vram_budget_mib;
+    p->preds.assign(n_tools, {});
+    for (int32_t e = 0; e < n_edges; ++e) {
+      const int32_t u = edges[e].src, v = edges[e].dst;
+      if (u < 0 || u >= n_tools || v < 0 || v >= n_tools || u == v) {
+        delete p;
+        return SCHED_E_EDGE;
+      }
+      p->preds[v].push_back(u);
+    }
+    int32_t total = 0;
+    for (auto& pl : p->preds) {
+      std::sort(pl.begin(), pl.end());
+      pl.erase(std::unique(pl.begin(), pl.end()), pl.end());
+      total += int32_t(pl.size());
+    }
+    p->n_preds = total;
+    // Kahn's algorithm: every tool must be reachable in a topological order.
+    std::vector<int32_t> indeg(n_tools, 0);
+    std::vector<std::vector<int32_t>> succ(n_tools);
+    for (int32_t v = 0; v < n_tools; ++v)
+      for (int32_t u : p->preds[v]) {
+        succ[u].push_back(v);
+        indeg[v]++;
+      }
+    std::vector<int32_t> stack;
+    for (int32_t v = 0; v < n_tools; ++v)
+      if (indeg[v] == 0) stack.push_back(v);
+    int32_t seen = 0;
+    while (!stack.empty()) {
+      const int32_t u = stack.back();
+      stack.pop_back();
+      ++seen;
+      for (int32_t v : succ[u])
+        if (--indeg[v] == 0) stack.push_back(v);
+    }
+    if (seen != n_tools) {
+      delete p;
+      return SCHED_E_CYCLE;
+    }
+    p->n_mappings = pow3(n_tools);
+    p->table_words = table_words(n_tools, total, std::min<int>(n_levels, n_tools));
+    p->table.assign(p->table_words, 0u);
+    const int rc = build_table(*p, nullptr, p->table.data());
+    if (rc != SCHED_OK) {
+      delete p;
+      return rc;
+    }
+  } catch (const std::bad_alloc&) {
+    delete p;
+    return SCHED_E_NOMEM;
+  }
+  *out = p;
+  return SCHED_OK;
+}
+
+void sched_problem_destroy(sched_problem* p) { delete p; }
+
+int sched_num_tools(const sched_problem* p, int32_t* out) {
+  if (p == nullptr || out == nullptr) return SCHED_E_NULL;
+  *out = p->n;
+  return SCHED_OK;
+}
+
+int sched_num_mappings(const sched_problem* p, uint64_t* out) {
+  if (p == nullptr || out == nullptr) return SCHED_E_NULL;
+  *out = p->n_mappings;
+  return SCHED_OK;
+}
+
+int sched_workspace_bytes(const sched_problem* const* problems, int32_t n_problems,
+                          int32_t n_replicas, size_t* out) {
+  if (problems == nullptr || out == nullptr) return SCHED_E_NULL;
+  if (n_problems < 1 || n_replicas < 0) return SCHED_E_SIZE;
+  size_t max_stride = 0;
+  for (int32_t i = 0; i < n_problems; ++i) {
+    if (problems[i] == nullptr) return SCHED_E_NULL;
+    max_stride = std::max<size_t>(max_stride, problems[i]->table_words);
+  }
+  // single-problem calls
+  size_t need = layout_for(max_stride * 4, partial_capacity(1), 1).total;
+  if (n_replicas > 0) {
+    const size_t r = size_t(n_replicas);
+    need = std::max(need, layout_for(r * max_stride * 4, partial_capacity(r), r).total);
+  }
+  *out = need;
+  return SCHED_OK;
+}
+
+int sched_bruteforce_argmin(const sched_problem* p, uint64_t lo, uint64_t hi, void* d_workspace,
+                            size_t ws_bytes, void* hip_stream, sched_result* h_out) {
+  if (p == nullptr || h_out == nullptr) return SCHED_E_NULL;
+  if (lo >= hi || hi > p->n_mappings) return SCHED_E_RANGE;
+  const Layout L = layout_for(size_t(p->table_words) * 4, partial_capacity(1), 1);
+  int rc = check_workspace(d_workspace, ws_bytes, L.total);
+  if (rc != SCHED_OK) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  char* ws = static_cast<char*>(d_workspace);
+
+  SearchArgs a{};
+  plan_search(p->n, lo, hi, 1, a);
+  a.tables = reinterpret_cast<const uint32_t*>(ws + L.tables);
+  a.table_stride = p->table_words;
+  a.partials = reinterpret_cast<Partial*>(ws + L.partials);
+  DevResult* d_res = reinterpret_cast<DevResult*>(ws + L.results);
+
+  HIP_TRY(hipMemcpyAsync(ws + L.tables, p->table.data(), size_t(p->table_words) * 4,
+                         hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_search(p->n, a, s));
+  HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, 1, d_res, s));
+  DevResult r;
+  HIP_TRY(hipMemcpyAsync(&r, d_res, sizeof(r), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  h_out->best_index = r.index;
+  h_out->makespan_us = r.makespan;
+  return SCHED_OK;
+}
+
+int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
+                     const int32_t* replica_problem, const sched_lat* replica_lat,
+                     int32_t n_replicas, void* d_workspace, size_t ws_bytes, void* hip_stream,
+                     sched_result* h_out) {
+  if (problems == nullptr || replica_problem == nullptr || replica_lat == nullptr ||
+      h_out == nullptr)
+    return SCHED_E_NULL;
+  if (n_problems < 1 || n_replicas < 1) return SCHED_E_SIZE;
+  size_t max_stride = 0;
+  for (int32_t i = 0; i < n_problems; ++i) {
+    if (problems[i] == nullptr) return SCHED_E_NULL;
+    max_stride = std::max<size_t>(max_stride, problems[i]->table_words);
+  }
+  std::vector<size_t> lat_off(static_cast<size_t>(n_replicas));
+  size_t off = 0;
+  for (int32_t r = 0; r < n_replicas; ++r) {
+    const int32_t pi = replica_problem[r];
+    if (pi < 0 || pi >= n_problems) return SCHED_E_RANGE;
+    lat_off[r] = off;
+    off += size_t(problems[pi]->n);
+  }
+  const size_t R = size_t(n_replicas);
+  const Layout L = layout_for(R * max_stride * 4, partial_capacity(R), R);
+  int rc = check_workspace(d_workspace, ws_bytes, L.total);
+  if (rc != SCHED_OK) return rc;
+
+  // Replicas grouped by tool count (one kernel instantiation per count).
+  std::vector<int32_t> order(R);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
+    return problems[replica_problem[x]]->n < problems[replica_problem[y]]->n;
+  });
+  std::vector<uint32_t> host_tables;
+  std::vector<DevResult> host_res;
+  try {
+    host_tables.assign(R * max_stride, 0u);
+    host_res.resize(R);
+  } catch (const std::bad_alloc&) {
+    return SCHED_E_NOMEM;
+  }
+  for (size_t i = 0; i < R; ++i) {
+    const int32_t r = order[i];
+    const sched_problem& p = *problems[replica_problem[r]];
+    rc = build_table(p, replica_lat + lat_off[r], host_tables.data() + i * max_stride);
+    if (rc != SCHED_OK) return rc;
+  }
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  char* ws = static_cast<char*>(d_workspace);
+  const uint32_t* d_tables = reinterpret_cast<const uint32_t*>(ws + L.tables);
+  Partial* d_partials = reinterpret_cast<Partial*>(ws + L.partials);
+  DevResult* d_res = reinterpret_cast<DevResult*>(ws + L.results);
+  HIP_TRY(hipMemcpyAsync(ws + L.tables, host_tables.data(), R * max_stride * 4,
+                         hipMemcpyHostToDevice, s));
+  size_t first = 0, partial_cursor = 0;
+  while (first < R) {
+    const int n = problems[replica_problem[order[first]]]->n;
+    size_t last = first;
+    while (last < R && problems[replica_problem[order[last]]]->n == n) ++last;
+    const uint32_t count = uint32_t(last - first);
+    SearchArgs a{};
+    // The block cap is shared by the whole batch so partials stay bounded.
+    plan_search(n, 0, pow3(n), count, a);
+    const uint64_t cap = std::max<uint64_t>(1, kMaxBlocks / R);
+    a.blocks_per_table = uint32_t(std::min<uint64_t>(a.items_per_table, cap));
+    a.tables = d_tables + first * max_stride;
+    a.table_stride = uint32_t(max_stride);
+    a.partials = d_partials + partial_cursor;
+    HIP_TRY(launch_search(n, a, s));
+    HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, count, d_res + first, s));
+    partial_cursor += size_t(count) * a.blocks_per_table;
+    first = last;
+  }
+  HIP_TRY(hipMemcpyAsync(host_res.data(), d_res, R * sizeof(DevResult), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  for (size_t i = 0; i < R; ++i) {
+    h_out[order[i]].best_index = host_res[i].index;
+    h_out[order[i]].makespan_us = host_res[i].makespan;
+  }
+  return SCHED_OK;
+}
+
+int sched_eval_mappings(const sched_problem* p, const uint64_t* d_idx, int64_t n,
+                        int64_t* d_makespan, void* d_workspace, size_t ws_bytes,
+                        void* hip_stream) {
+  if (p == nullptr) return SCHED_E_NULL;
+  if (n < 0) return SCHED_E_SIZE;
+  if (n == 0) return SCHED_OK;
+  if (d_idx == nullptr || d_makespan == nullptr) return SCHED_E_NULL;
+  const size_t need = align_up(size_t(p->table_words) * 4);
+  int rc = check_workspace(d_workspace, ws_bytes, need);
+  if (rc != SCHED_OK) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  HIP_TRY(hipMemcpyAsync(d_workspace, p->table.data(), size_t(p->table_words) * 4,
+                         hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_eval(p->n, static_cast<const uint32_t*>(d_workspace), d_idx, n, p->n_mappings,
+                      d_makespan, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return SCHED_OK;
+}
+
+const char* sched_strerror(int code) {
+  switch (code) {
+    case SCHED_OK: return "ok";
+    case SCHED_E_NULL: return "null pointer argument";
+    case SCHED_E_SIZE: return "size out of range";
+    case SCHED_E_VALUE: return "value out of range";
+    case SCHED_E_EDGE: return "edge endpoint out of range or self-loop";
+    case SCHED_E_CYCLE: return "edges contain a cycle";
+    case SCHED_E_RANGE: return "index range or replica map out of range";
+    case SCHED_E_OVERFLOW: return "times or VRAM sums would not fit the 32-bit device path";
+    case SCHED_E_WORKSPACE: return "workspace null, misaligned or too small";
+    case SCHED_E_DEVICE: return "HIP runtime error";
+    case SCHED_E_NOMEM: return "host allocation failed";
+    default: return "unknown error";
+  }
+}
+
+}  // extern "C"

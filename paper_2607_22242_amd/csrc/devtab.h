@@ -1,0 +1,78 @@
+// devtab.h -- device-side problem table and launch arguments (internal).
+//
+// One table per problem (or per replica in a batch) is a flat array of
+// 32-bit words, written by the host into the caller's workspace and read by
+// the kernels with uniform (scalar) loads, except the duration table which
+// each block stages in LDS because its index depends on the lane.
+#pragma once
+#include <stdint.h>
+
+namespace devmap {
+
+constexpr int kMaxTools = 40;
+constexpr int kMaxLevels = 64;
+constexpr uint32_t kInf = 0xFFFFFFFFu;  // "never": unknown ready time, infeasible
+constexpr int kBlock = 256;             // threads per search block (4 waves)
+constexpr int kMaxInnerDigits = 6;      // inner (wave-uniform) digits per lane
+
+// Header words.
+enum : uint32_t {
+  kHdrN = 0,          // number of tools
+  kHdrLevels = 1,     // contention levels stored = min(K, N)
+  kHdrBudget = 2,     // VRAM budget, clamped to the summed footprint
+  kHdrBigLo = 3,      // tools whose footprint exceeds the budget (bits 0..31)
+  kHdrBigHi = 4,      //                                           (bits 32..63)
+  kHdrSrcLo = 5,      // tools without predecessors
+  kHdrSrcHi = 6,
+  kHdrDurOff = 7,     // word offset of the duration table
+  kHdrWords = 16,
+};
+
+// Per-tool record at kHdrWords + kToolWords * v.
+enum : uint32_t {
+  kToolCpu = 0,       // cpu_us
+  kToolMem = 1,       // footprint, clamped to budget + 1
+  kToolXfer = 2,      // input transfer across devices
+  kToolPredLo = 3,    // predecessor mask bits 0..31
+  kToolPredHi = 4,    // predecessor mask bits 32..63
+  kToolPredOff = 5,   // offset of the predecessor list (from kPredBase)
+  kToolNPred = 6,     // number of predecessors
+  kToolWords = 8,
+};
+
+constexpr uint32_t kPredBase = kHdrWords + kToolWords * kMaxTools;  // 336
+
+// Duration table: dur[(v * 2 + q) * levels + (level - 1)], q = 0 for
+// gpu_now (base gpu_us), q = 1 for gpu_queue (base gpu_us + load_us).
+
+inline uint32_t table_words(int n, int n_preds, int levels) {
+  uint32_t dur_off = kPredBase + ((uint32_t(n_preds) + 3u) & ~3u);
+  return dur_off + uint32_t(n) * 2u * uint32_t(levels);
+}
+
+struct Partial {
+  uint64_t index;
+  uint32_t makespan;
+  uint32_t pad;
+};
+
+struct SearchArgs {
+  const uint32_t* tables;     // n_tables tables, table_stride words apart
+  Partial* partials;          // one per block
+  uint64_t lo, hi;            // index range searched in every table
+  uint64_t outer_lo;          // first outer combination
+  uint64_t n_outer;           // outer combinations covering [lo, hi)
+  uint32_t table_stride;
+  uint32_t n_tables;
+  uint32_t inner_digits;      // J: tools 0..J-1 are enumerated per lane
+  uint32_t inner_count;       // 3^J
+  uint64_t items_per_table;   // ceil(n_outer / kBlock)
+  uint32_t blocks_per_table;
+};
+
+struct DevResult {
+  uint64_t index;
+  int64_t makespan;
+};
+
+}  // namespace devmap

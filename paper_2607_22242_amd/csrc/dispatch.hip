@@ -1,0 +1,97 @@
+// dispatch.hip -- run-time dispatch on the tool count, and the final
+// per-table argmin reduction.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <array>
+#include <utility>
+
+#include "devtab.h"
+#include "launch.h"
+
+namespace devmap {
+
+template <int N>
+hipError_t launch_search_n(const SearchArgs& a, hipStream_t s);
+template <int N>
+hipError_t launch_eval_n(const uint32_t* tab, const uint64_t* idx, int64_t n, uint64_t n_mappings,
+                         int64_t* out, hipStream_t s);
+
+__device__ __forceinline__ void lex_min(uint32_t& ms, uint64_t& x, uint32_t oms, uint64_t ox) {
+  if (oms < ms || (oms == ms && ox < x)) {
+    ms = oms;
+    x = ox;
+  }
+}
+
+// Block-wide lexicographic min of (makespan, index); result valid in thread 0.
+__device__ __forceinline__ void block_min(uint32_t& ms, uint64_t& x) {
+  __shared__ uint32_t s_ms[kBlock / 64];
+  __shared__ uint64_t s_x[kBlock / 64];
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t oms = __shfl_xor(ms, off);
+    const uint64_t ox = __shfl_xor(x, off);
+    lex_min(ms, x, oms, ox);
+  }
+  const int wave = threadIdx.x / 64;
+  if ((threadIdx.x & 63) == 0) {
+    s_ms[wave] = ms;
+    s_x[wave] = x;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kBlock / 64; ++w) lex_min(ms, x, s_ms[w], s_x[w]);
+  }
+}
+
+// Per-table minimum over its blocks' partials.
+__global__ __launch_bounds__(kBlock) void reduce_kernel(const Partial* __restrict__ partials,
+                                                        uint32_t per_table,
+                                                        DevResult* __restrict__ out) {
+  const Partial* p = partials + size_t(blockIdx.x) * per_table;
+  uint32_t ms = kInf;
+  uint64_t x = ~0ull;
+  for (uint32_t i = threadIdx.x; i < per_table; i += kBlock) lex_min(ms, x, p[i].makespan, p[i].index);
+  block_min(ms, x);
+  if (threadIdx.x == 0) {
+    DevResult r;
+    r.index = (ms == kInf) ? ~0ull : x;
+    r.makespan = (ms == kInf) ? INT64_MAX : int64_t(ms);
+    out[blockIdx.x] = r;
+  }
+}
+
+using SearchFn = hipError_t (*)(const SearchArgs&, hipStream_t);
+using EvalFn = hipError_t (*)(const uint32_t*, const uint64_t*, int64_t, uint64_t, int64_t*,
+                              hipStream_t);
+
+template <size_t... I>
+static constexpr auto make_search_table(std::index_sequence<I...>) {
+  return std::array<SearchFn, sizeof...(I)>{&launch_search_n<int(I) + 1>...};
+}
+template <size_t... I>
+static constexpr auto make_eval_table(std::index_sequence<I...>) {
+  return std::array<EvalFn, sizeof...(I)>{&launch_eval_n<int(I) + 1>...};
+}
+
+static const auto kSearchFns = make_search_table(std::make_index_sequence<kMaxTools>{});
+static const auto kEvalFns = make_eval_table(std::make_index_sequence<kMaxTools>{});
+
+hipError_t launch_search(int n_tools, const SearchArgs& a, hipStream_t s) {
+  return kSearchFns[n_tools - 1](a, s);
+}
+
+hipError_t launch_eval(int n_tools, const uint32_t* tab, const uint64_t* idx, int64_t n,
+                       uint64_t n_mappings, int64_t* out, hipStream_t s) {
+  return kEvalFns[n_tools - 1](tab, idx, n, n_mappings, out, s);
+}
+
+hipError_t launch_reduce(const Partial* partials, uint32_t per_table, uint32_t n_tables,
+                         DevResult* out, hipStream_t s) {
+  hipLaunchKernelGGL(reduce_kernel, dim3(n_tables), dim3(kBlock), 0, s, partials, per_table,
+                     out);
+  return hipGetLastError();
+}
+
+}  // namespace devmap

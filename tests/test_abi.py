@@ -1,0 +1,106 @@
+"""The C ABI on the host: exported symbols and validation (no device work)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_22242_amd as S
+from paper_2607_22242_amd import binding as B
+from workloads import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sched_search.h")
+F = [65536, 88474, 117965, 157286]
+TOOL = [1000, 2000, 100, 10, 512]
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sched_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert names == sorted(B.EXPORTED)
+    L = ctypes.CDLL(B.LIB_PATH)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def err(fn, *a):
+    with pytest.raises(S.SchedError) as e:
+        fn(*a)
+    return e.value.name
+
+
+def test_create_validation():
+    c = S.sched_problem_create
+    assert err(c, [TOOL] * 41, [], F, 100) == "SCHED_E_SIZE"
+    assert err(c, [TOOL], [], [], 100) == "SCHED_E_SIZE"
+    assert err(c, [TOOL], [], [65536] * 65, 100) == "SCHED_E_SIZE"
+    assert err(c, [[0, 1, 0, 0, 1]], [], F, 100) == "SCHED_E_VALUE"      # gpu_us < 1
+    assert err(c, [[1, 0, 0, 0, 1]], [], F, 100) == "SCHED_E_VALUE"      # cpu_us < 1
+    assert err(c, [[1, 1, -1, 0, 1]], [], F, 100) == "SCHED_E_VALUE"
+    assert err(c, [[1, 1, 0, -1, 1]], [], F, 100) == "SCHED_E_VALUE"
+    assert err(c, [[1, 1, 0, 0, -1]], [], F, 100) == "SCHED_E_VALUE"
+    assert err(c, [TOOL], [], F, -1) == "SCHED_E_VALUE"
+    assert err(c, [TOOL], [], [65535], 100) == "SCHED_E_VALUE"           # below 1.0x
+    assert err(c, [TOOL], [], [(1 << 24) + 1], 100) == "SCHED_E_VALUE"
+    assert err(c, [TOOL] * 2, [[0, 2]], F, 100) == "SCHED_E_EDGE"
+    assert err(c, [TOOL] * 2, [[1, 1]], F, 100) == "SCHED_E_EDGE"
+    assert err(c, [TOOL] * 2, [[-1, 1]], F, 100) == "SCHED_E_EDGE"
+    assert err(c, [TOOL] * 3, [[0, 1], [1, 2], [2, 0]], F, 100) == "SCHED_E_CYCLE"
+    # times beyond the 32-bit device guard
+    assert err(c, [[1 << 31, 1, 0, 0, 1]], [], F, 100) == "SCHED_E_OVERFLOW"
+    assert err(c, [[1, 1 << 31, 0, 0, 1]], [], F, 100) == "SCHED_E_OVERFLOW"
+    assert err(c, [[1000, 1000, 0, 0, 1 << 40]] * 2, [], F, 1 << 40) == "SCHED_E_OVERFLOW"
+    # duplicates are ignored, N = 40 accepted
+    P = S.Problem([TOOL] * 2, [[0, 1], [0, 1]], F, 100)
+    assert P.n_mappings == 9
+    P = S.Problem([TOOL] * 40, [], F, 100)
+    assert P.n == 40 and P.n_mappings == 3 ** 40
+
+
+def test_workspace_and_range_validation_before_any_device_work():
+    P = S.Problem.from_instance(synth.load(0))
+    nbytes = S.sched_workspace_bytes([P.handle])
+    assert nbytes > 0 and nbytes % 256 == 0
+    assert S.sched_workspace_bytes([P.handle], 832) > nbytes
+
+    class FakeWs:  # host validation never dereferences the workspace
+        def __init__(self, ptr, n):
+            self.p, self.n = ptr, n
+
+        def data_ptr(self):
+            return self.p
+
+        def numel(self):
+            return self.n
+
+        def element_size(self):
+            return 1
+
+    class FakeStream:
+        cuda_stream = 0
+
+    fs = FakeStream()
+    r = lambda lo, hi, ws: S.sched_bruteforce_argmin(P.handle, lo, hi, ws, fs)  # noqa: E731
+    assert err(r, 5, 5, FakeWs(256, nbytes)) == "SCHED_E_RANGE"
+    assert err(r, 0, 3 ** 8 + 1, FakeWs(256, nbytes)) == "SCHED_E_RANGE"
+    assert err(r, 0, 3 ** 8, FakeWs(0, nbytes)) == "SCHED_E_WORKSPACE"
+    assert err(r, 0, 3 ** 8, FakeWs(128, nbytes)) == "SCHED_E_WORKSPACE"
+    assert err(r, 0, 3 ** 8, FakeWs(256, nbytes - 256)) == "SCHED_E_WORKSPACE"
+    b = lambda rp, ws: S.sched_eval_batch([P.handle], rp, [synth.load(0)["tools"]], ws, fs)  # noqa
+    assert err(b, [1], FakeWs(256, 1 << 30)) == "SCHED_E_RANGE"
+    assert err(b, [0], FakeWs(256, 64)) == "SCHED_E_WORKSPACE"
+    bad_lat = [[0, 1, 0, 0]] * 8
+    assert err(lambda: S.sched_eval_batch([P.handle], [0], [bad_lat], FakeWs(256, 1 << 30),
+                                          fs)) == "SCHED_E_VALUE"
+
+
+def test_strerror_covers_codes():
+    for code, name in B.ERRORS.items():
+        assert S.sched_strerror(code) != "unknown error", name
+    assert S.sched_strerror(0) == "ok"

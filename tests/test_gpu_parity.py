@@ -1,0 +1,261 @@
+"""GPU parity: the HIP library against the CPU oracle, bit-exact.
+
+Every comparison is exact (integer makespans and indices).  Full-size
+searches (3^19 mappings, 832 x 3^14) compare with expected values written by
+tests/golden/make_expected.py from the oracle alone, and the returned
+mapping is re-scored by the oracle.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import paper_2607_22242_amd as S
+from workloads import synth
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+INF64 = (1 << 63) - 1
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    return torch
+
+
+@pytest.fixture(scope="module")
+def O(oracle_mod):
+    return oracle_mod
+
+
+@pytest.fixture(scope="module")
+def expected():
+    with open(os.path.join(GOLDEN, "expected_configs.json")) as f:
+        return json.load(f)
+
+
+def gpu_eval(torch, P, idx):
+    idx = np.ascontiguousarray(np.asarray(idx, dtype=np.uint64))
+    d_idx = torch.from_numpy(idx.view(np.int64)).to("cuda")
+    d_out = torch.empty(len(idx), dtype=torch.int64, device="cuda")
+    ws = S.workspace([P.handle])
+    S.sched_eval_mappings(P.handle, d_idx, d_out, ws)
+    return d_out.cpu().numpy()
+
+
+def gpu_argmin(torch, P, lo=0, hi=None):
+    ws = S.workspace([P.handle])
+    return S.sched_bruteforce_argmin(P.handle, lo, P.n_mappings if hi is None else hi, ws)
+
+
+def both(inst, O):
+    return S.Problem.from_instance(inst), O.Problem.from_instance(inst)
+
+
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("c", [0, 1])
+def test_every_index_small_configs(torch_cuda, O, c):
+    P, Q = both(synth.load(c), O)
+    idx = np.arange(P.n_mappings, dtype=np.uint64)
+    say(f"eval_mappings config {c}: {len(idx)} indices")
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, idx), Q.eval_many(idx))
+
+
+@pytest.mark.parametrize("c", [2, 3])
+def test_sampled_indices_large_configs(torch_cuda, O, c):
+    P, Q = both(synth.load(c), O)
+    rng = np.random.default_rng(77 + c)
+    idx = np.concatenate([rng.integers(0, P.n_mappings, 200000, dtype=np.uint64),
+                          np.array([0, 1, P.n_mappings - 1], dtype=np.uint64)])
+    say(f"eval_mappings config {c}: {len(idx)} sampled indices")
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, idx), Q.eval_many(idx))
+
+
+def test_out_of_range_indices_are_infeasible(torch_cuda, O):
+    P, Q = both(synth.load(0), O)
+    idx = np.array([3 ** 8, 3 ** 8 + 5, (1 << 64) - 1, 7], dtype=np.uint64)
+    say("eval_mappings out-of-range indices")
+    got = gpu_eval(torch_cuda, P, idx)
+    assert list(got[:3]) == [INF64] * 3 and got[3] == Q.eval_index(7)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_dags_every_index(torch_cuda, O, seed):
+    n = 1 + seed % 8
+    shape = ["random", "chain", "fanout"][seed % 3]
+    inst = synth.random_instance(2000 + seed, n, shape, levels=1 + seed % 5,
+                                 tight=(seed % 2 == 0), small_values=(seed % 4 == 1))
+    P, Q = both(inst, O)
+    idx = np.arange(3 ** n, dtype=np.uint64)
+    say(f"random dag seed {seed} n {n} {shape}")
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, idx), Q.eval_many(idx, threads=1))
+    assert gpu_argmin(torch_cuda, P) == Q.argmin(threads=1)
+
+
+@pytest.mark.parametrize("c", [0, 1, 2])
+def test_full_search_small_configs(torch_cuda, O, expected, c):
+    P, Q = both(synth.load(c), O)
+    say(f"argmin config {c}")
+    got = gpu_argmin(torch_cuda, P)
+    e = expected[f"config{c}"]
+    assert got == (e["best_index"], e["makespan_us"])
+    if c < 2:
+        assert got == Q.argmin()
+    assert Q.eval_index(got[0]) == got[1]
+
+
+def test_full_search_mixed19(torch_cuda, O, expected):
+    """3^19 = 1,162,261,467 mappings, the bench's launch configuration."""
+    if "config3" not in expected:
+        pytest.skip("expected value for the 3^19 search not generated yet")
+    P, Q = both(synth.load(3), O)
+    say("argmin config 3 (3^19)")
+    got = gpu_argmin(torch_cuda, P)
+    assert got == (expected["config3"]["best_index"], expected["config3"]["makespan_us"])
+    assert Q.eval_index(got[0]) == got[1]
+    # sampled mappings are never better than the reported optimum
+    rng = np.random.default_rng(3)
+    sample = Q.eval_many(rng.integers(0, P.n_mappings, 100000, dtype=np.uint64))
+    assert sample.min() >= got[1]
+
+
+def batch_inputs(inst):
+    scen = inst["scenarios"]
+    problems = [S.Problem.from_instance(s) for s in scen]
+    rp, lat = [], []
+    for si, s in enumerate(scen):
+        for rep in s["replicas"]:
+            rp.append(si)
+            lat.append(rep)
+    return problems, rp, lat
+
+
+def test_batch_rescoring_full(torch_cuda, O, expected):
+    """13 scenarios x 64 replicas x 3^14 mappings in one call."""
+    if "config4" not in expected:
+        pytest.skip("expected values for the batched search not generated yet")
+    inst = synth.load(4)
+    problems, rp, lat = batch_inputs(inst)
+    ws = S.workspace([p.handle for p in problems], len(rp))
+    say("eval_batch config 4 (832 x 3^14)")
+    got = S.sched_eval_batch([p.handle for p in problems], rp, lat, ws)
+    want = [tuple(x) for row in expected["config4"]["results"] for x in row]
+    assert got == want
+    for r in range(0, len(rp), 37):  # re-score a spread of replicas
+        Q = O.Problem.from_instance(inst["scenarios"][rp[r]], lat[r])
+        assert Q.eval_index(got[r][0]) == got[r][1]
+
+
+def test_batch_matches_oracle_small_mixed_sizes(torch_cuda, O):
+    insts = [synth.random_instance(3000 + i, n, sh, levels=3, tight=(i % 2 == 0))
+             for i, (n, sh) in enumerate([(3, "random"), (6, "chain"), (5, "fanout"),
+                                          (7, "random"), (6, "random")])]
+    problems = [S.Problem.from_instance(i) for i in insts]
+    rng = np.random.default_rng(9)
+    rp, lat = [], []
+    for r in range(40):
+        p = int(rng.integers(0, len(insts)))
+        rp.append(p)
+        lat.append(synth.perturb(insts[p]["tools"], 4000 + r))
+    ws = S.workspace([p.handle for p in problems], len(rp))
+    say("eval_batch mixed sizes")
+    got = S.sched_eval_batch([p.handle for p in problems], rp, lat, ws)
+    for r in range(len(rp)):
+        Q = O.Problem.from_instance(insts[rp[r]], lat[r])
+        assert got[r] == Q.argmin(threads=1), r
+
+
+@pytest.mark.parametrize("c", [1, 2])
+def test_ragged_ranges(torch_cuda, O, c):
+    P, Q = both(synth.load(c), O)
+    rng = np.random.default_rng(c)
+    total = P.n_mappings
+    cases = [(0, 1), (total - 1, total), (255, 257), (1000, 1000 + 3 ** 6 + 13),
+             (12345, 12345 + 256 * 7 + 3)]
+    for _ in range(6):
+        lo = int(rng.integers(0, total))
+        hi = int(rng.integers(lo + 1, min(total, lo + 4_000_000) + 1))
+        cases.append((lo, hi))
+    for lo, hi in cases:
+        say(f"argmin config {c} range [{lo}, {hi})")
+        assert gpu_argmin(torch_cuda, P, lo, hi) == Q.argmin(lo, hi), (lo, hi)
+
+
+@pytest.mark.parametrize("n", [20, 21, 24, 32, 33, 40])
+def test_wide_problems_64bit_indices(torch_cuda, O, n):
+    inst = synth.random_instance(5000 + n, n, "random", levels=4, tight=True, small_values=True)
+    P, Q = both(inst, O)
+    rng = np.random.default_rng(n)
+    idx = rng.integers(0, min(P.n_mappings, (1 << 63) - 1), 20000, dtype=np.uint64)
+    idx = np.concatenate([idx, np.array([P.n_mappings - 1, 0], dtype=np.uint64)])
+    say(f"eval_mappings n={n}")
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, idx), Q.eval_many(idx))
+    lo = P.n_mappings - 3 ** 9 - 17
+    say(f"argmin n={n} top range")
+    assert gpu_argmin(torch_cuda, P, lo, P.n_mappings) == Q.argmin(lo, P.n_mappings)
+    lo = (P.n_mappings // 7) * 3
+    assert gpu_argmin(torch_cuda, P, lo, lo + 50000) == Q.argmin(lo, lo + 50000)
+
+
+def test_paper_scenarios_on_gpu(torch_cuda, O):
+    with open(os.path.join(GOLDEN, "paper_scenarios.json")) as f:
+        d = json.load(f)
+    for name, s in d["scenarios"].items():
+        edges = d["diamond_edges"] if s["topology"] == "diamond" else []
+        P = S.Problem(s["tools"], edges, d["contention_q16"], s["budget"])
+        Q = O.Problem(s["tools"], edges, d["contention_q16"], s["budget"])
+        say(f"paper scenario {name}")
+        got = gpu_argmin(torch_cuda, P)
+        assert got == Q.argmin(threads=1)
+        if s["expect"] == "match":
+            assert O.modes_of(got[0], 4) == s["paper_oracle"]
+        np.testing.assert_array_equal(gpu_eval(torch_cuda, P, np.arange(81)),
+                                      Q.eval_many(np.arange(81, dtype=np.uint64)))
+
+
+def test_degenerate_cases(torch_cuda, O):
+    say("degenerate: single tool")
+    P = S.Problem([[100, 300, 50, 0, 10]], [], [65536, 98304], 16)
+    assert gpu_argmin(torch_cuda, P) == (1, 100)
+    assert gpu_argmin(torch_cuda, P, 2, 3) == (2, 150)
+    say("degenerate: zero budget")
+    inst = dict(synth.load(1), vram_budget_mib=0)
+    P, Q = both(inst, O)
+    assert gpu_argmin(torch_cuda, P) == (0, Q.eval_index(0))
+    say("degenerate: no feasible mapping in range")
+    assert gpu_argmin(torch_cuda, P, 1, 3 ** 6) == (S.NO_INDEX, INF64)
+    say("degenerate: every GPU mode infeasible")
+    inst = synth.random_instance(6000, 6, "random")
+    inst["vram_budget_mib"] = min(t[4] for t in inst["tools"]) - 1
+    P, Q = both(inst, O)
+    assert gpu_argmin(torch_cuda, P) == Q.argmin() == (0, Q.eval_index(0))
+    say("degenerate: single-level table, unconstrained budget")
+    inst = synth.random_instance(6001, 9, "fanout", levels=1)
+    inst["vram_budget_mib"] = 1 << 20
+    P, Q = both(inst, O)
+    assert gpu_argmin(torch_cuda, P) == Q.argmin()
+
+
+def test_exact_workspace_and_repeat_calls(torch_cuda, O):
+    P, Q = both(synth.load(2), O)
+    nbytes = S.sched_workspace_bytes([P.handle])
+    raw = torch_cuda.empty(nbytes + 256, dtype=torch_cuda.uint8, device="cuda")
+    off = (-raw.data_ptr()) % 256
+    ws = raw[off:off + nbytes]
+    assert ws.numel() == nbytes
+    say("argmin config 2 with an exact-size workspace, twice, on a side stream")
+    s = torch_cuda.cuda.Stream()
+    a = S.sched_bruteforce_argmin(P.handle, 0, P.n_mappings, ws, s)
+    b = S.sched_bruteforce_argmin(P.handle, 0, P.n_mappings, ws)
+    assert a == b
