@@ -18,6 +18,7 @@ struct sched_problem {
   int32_t n = 0;
   std::vector<sched_tool> tools;
   std::vector<std::vector<int32_t>> preds;  // ascending, deduplicated
+  std::vector<int32_t> order;               // order[i]: original tool with internal label i
   std::vector<uint32_t> contention;         // F[k-1]
   int64_t budget = 0;
   uint64_t n_mappings = 0;
@@ -67,11 +68,14 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
   if ((unsigned __int128)(n + 1) * (unsigned __int128)(budget + 1) >= ((unsigned __int128)1 << 32))
     return SCHED_E_OVERFLOW;
 
-  uint64_t big = 0, src = 0;
+  std::vector<int32_t> label(n);
+  for (int i = 0; i < n; ++i) label[p.order[i]] = i;
+  uint64_t big = 0;
   unsigned __int128 bound = 0;  // worst-case makespan: sum of longest durations + transfers
   const uint32_t dur_off = kPredBase + ((uint32_t(p.n_preds) + 3u) & ~3u);
   uint32_t pred_cursor = 0;
-  for (int v = 0; v < n; ++v) {
+  for (int i = 0; i < n; ++i) {
+    const int v = p.order[i];
     const sched_tool& tl = p.tools[v];
     const int64_t gpu = lat ? lat[v].gpu_us : tl.gpu_us;
     const int64_t cpu = lat ? lat[v].cpu_us : tl.cpu_us;
@@ -85,33 +89,36 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
       for (int l = 0; l < levels; ++l) {
         const uint64_t d = scale_q16(base, p.contention[l]);
         longest = std::max(longest, d);
-        if (d < (1ull << 31)) out[dur_off + (uint32_t(v) * 2u + uint32_t(q)) * uint32_t(levels) + l] = uint32_t(d);
+        if (d < (1ull << 31))
+          out[dur_off + (uint32_t(i) * 2u + uint32_t(q)) * uint32_t(levels) + l] = uint32_t(d);
       }
     }
     bound += (unsigned __int128)longest + (unsigned __int128)uint64_t(xfer);
     if (bound >= ((unsigned __int128)1 << 31)) return SCHED_E_OVERFLOW;
 
-    uint32_t* rec = out + kHdrWords + kToolWords * uint32_t(v);
+    uint32_t* rec = out + kHdrWords + kToolWords * uint32_t(i);
     rec[kToolCpu] = uint32_t(cpu);
     rec[kToolMem] = uint32_t(std::min<int64_t>(tl.mem_mib, budget + 1));
     rec[kToolXfer] = uint32_t(xfer);
+    std::vector<int32_t> pl;
+    for (int32_t u : p.preds[v]) pl.push_back(label[u]);
+    std::sort(pl.begin(), pl.end());
     uint64_t pm = 0;
-    for (int32_t u : p.preds[v]) pm |= 1ull << u;
+    for (int32_t u : pl) pm |= 1ull << u;
     rec[kToolPredLo] = uint32_t(pm);
     rec[kToolPredHi] = uint32_t(pm >> 32);
     rec[kToolPredOff] = pred_cursor;
-    rec[kToolNPred] = uint32_t(p.preds[v].size());
-    for (int32_t u : p.preds[v]) out[kPredBase + pred_cursor++] = uint32_t(u);
-    if (tl.mem_mib > budget) big |= 1ull << v;
-    if (p.preds[v].empty()) src |= 1ull << v;
+    rec[kToolNPred] = uint32_t(pl.size());
+    rec[kToolOrig] = uint32_t(v);
+    for (int32_t u : pl) out[kPredBase + pred_cursor++] = uint32_t(u);
+    out[kPosBase + v] = uint32_t(i);
+    if (tl.mem_mib > budget) big |= 1ull << i;
   }
   out[kHdrN] = uint32_t(n);
   out[kHdrLevels] = uint32_t(levels);
   out[kHdrBudget] = uint32_t(budget);
   out[kHdrBigLo] = uint32_t(big);
   out[kHdrBigHi] = uint32_t(big >> 32);
-  out[kHdrSrcLo] = uint32_t(src);
-  out[kHdrSrcHi] = uint32_t(src >> 32);
   out[kHdrDurOff] = dur_off;
   return SCHED_OK;
 }
@@ -220,18 +227,19 @@ int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_e
         succ[u].push_back(v);
         indeg[v]++;
       }
-    std::vector<int32_t> stack;
-    for (int32_t v = 0; v < n_tools; ++v)
-      if (indeg[v] == 0) stack.push_back(v);
-    int32_t seen = 0;
-    while (!stack.empty()) {
-      const int32_t u = stack.back();
-      stack.pop_back();
-      ++seen;
-      for (int32_t v : succ[u])
-        if (--indeg[v] == 0) stack.push_back(v);
+    // Kahn's algorithm, always taking the lowest-numbered ready tool: the
+    // internal labels of the device tables (a cycle leaves tools unlabelled).
+    std::vector<char> done(n_tools, 0);
+    for (int32_t step = 0; step < n_tools; ++step) {
+      int32_t u = -1;
+      for (int32_t v = 0; v < n_tools && u < 0; ++v)
+        if (!done[v] && indeg[v] == 0) u = v;
+      if (u < 0) break;
+      done[u] = 1;
+      p->order.push_back(u);
+      for (int32_t v : succ[u]) --indeg[v];
     }
-    if (seen != n_tools) {
+    if (int32_t(p->order.size()) != n_tools) {
       delete p;
       return SCHED_E_CYCLE;
     }

@@ -4,6 +4,12 @@
 // 32-bit words, written by the host into the caller's workspace and read by
 // the kernels with uniform (scalar) loads, except the duration table which
 // each block stages in LDS because its index depends on the lane.
+//
+// Tools are stored under internal labels 0..N-1 that follow a topological
+// order of the DAG (every predecessor has a smaller label), so one ascending
+// sweep over the labels sees each tool after all of its predecessors.  The
+// mapping index keeps the caller's tool numbering: digit v of the index is
+// the mode of original tool v, whose internal label is pos[v].
 #pragma once
 #include <stdint.h>
 
@@ -22,13 +28,11 @@ enum : uint32_t {
   kHdrBudget = 2,     // VRAM budget, clamped to the summed footprint
   kHdrBigLo = 3,      // tools whose footprint exceeds the budget (bits 0..31)
   kHdrBigHi = 4,      //                                           (bits 32..63)
-  kHdrSrcLo = 5,      // tools without predecessors
-  kHdrSrcHi = 6,
-  kHdrDurOff = 7,     // word offset of the duration table
+  kHdrDurOff = 5,     // word offset of the duration table
   kHdrWords = 16,
 };
 
-// Per-tool record at kHdrWords + kToolWords * v.
+// Record of the tool with internal label i at kHdrWords + kToolWords * i.
 enum : uint32_t {
   kToolCpu = 0,       // cpu_us
   kToolMem = 1,       // footprint, clamped to budget + 1
@@ -37,13 +41,17 @@ enum : uint32_t {
   kToolPredHi = 4,    // predecessor mask bits 32..63
   kToolPredOff = 5,   // offset of the predecessor list (from kPredBase)
   kToolNPred = 6,     // number of predecessors
+  kToolOrig = 7,      // original tool number (queue ties go to the lowest)
   kToolWords = 8,
 };
 
-constexpr uint32_t kPredBase = kHdrWords + kToolWords * kMaxTools;  // 336
+// pos[v]: internal label of original tool v.
+constexpr uint32_t kPosBase = kHdrWords + kToolWords * kMaxTools;  // 336
+// Predecessor lists (internal labels), then the duration table.
+constexpr uint32_t kPredBase = kPosBase + kMaxTools;  // 376
 
-// Duration table: dur[(v * 2 + q) * levels + (level - 1)], q = 0 for
-// gpu_now (base gpu_us), q = 1 for gpu_queue (base gpu_us + load_us).
+// Duration table: dur[(i * 2 + q) * levels + (level - 1)] for internal label
+// i, q = 0 for gpu_now (base gpu_us), q = 1 for gpu_queue (gpu_us + load_us).
 
 inline uint32_t table_words(int n, int n_preds, int levels) {
   uint32_t dur_off = kPredBase + ((uint32_t(n_preds) + 3u) & ~3u);

@@ -31,6 +31,39 @@ using MaskT = typename std::conditional<(N <= 32), uint32_t, uint64_t>::type;
 #define DEVMAP_UNIFORM(x) (x)
 #endif
 
+// Read-only view of a problem table.  On the device it reads through the
+// constant address space, so wave-uniform reads become scalar loads.
+struct Tab {
+  const uint32_t* p;
+  __host__ __device__ __forceinline__ uint32_t operator[](uint32_t i) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    typedef const __attribute__((address_space(4))) uint32_t* ConstPtr;
+    return ((ConstPtr)p)[i];
+#else
+    return p[i];
+#endif
+  }
+  __host__ __device__ __forceinline__ Tab operator+(uint32_t i) const { return Tab{p + i}; }
+};
+
+// The table, opaque to the optimiser: reads through the returned view are
+// re-issued where they are used (scalar-cache hits) instead of being hoisted
+// out of the event loop into registers that would then spill.
+__host__ __device__ __forceinline__ Tab fresh(const uint32_t* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("" : "+s"(p));
+#endif
+  return Tab{p};
+}
+
+// An empty side effect: keeps a wave-uniform branch a branch instead of
+// letting the optimiser turn its body into per-lane selects.
+#if defined(__HIP_DEVICE_COMPILE__)
+#define DEVMAP_KEEP_BRANCH() asm volatile("")
+#else
+#define DEVMAP_KEEP_BRANCH() ((void)0)
+#endif
+
 __host__ __device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
 __host__ __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 
@@ -41,8 +74,8 @@ __host__ __device__ __forceinline__ MaskT<N> all_tools() {
   else return (MaskT<N>(1) << N) - 1;
 }
 
-template <int N>
-__host__ __device__ __forceinline__ MaskT<N> load_mask(const uint32_t* tab, uint32_t lo_word) {
+template <int N, class P>
+__host__ __device__ __forceinline__ MaskT<N> load_mask(const P& tab, uint32_t lo_word) {
   if constexpr (N <= 32) return tab[lo_word];
   else return uint64_t(tab[lo_word]) | (uint64_t(tab[lo_word + 1]) << 32);
 }
@@ -52,146 +85,182 @@ __host__ __device__ __forceinline__ bool bit(MaskT<N> m, int v) {
   return (m >> v) & 1;
 }
 
+// LDS image staged by every block: the duration table, then footprints by
+// internal label, then the internal label of every original tool.
+template <int N>
+constexpr uint32_t lds_levels() { return N < kMaxLevels ? N : kMaxLevels; }
+template <int N>
+constexpr uint32_t lds_mem_off() { return uint32_t(N) * 2u * lds_levels<N>(); }
+template <int N>
+constexpr uint32_t lds_pos_off() { return lds_mem_off<N>() + uint32_t(N); }
+template <int N>
+constexpr uint32_t lds_words() { return lds_pos_off<N>() + uint32_t(N); }
+
 // Makespan of one mapping under the schedule model, or kInf if infeasible.
 //
-// gnm / gqm: tools on gpu_now / gpu_queue (the rest run on the CPU).
-// T[v] holds tool v's ready time while it waits (kInf until all of its
-// predecessors have started) and its finish time once it has started.  Each
-// pass of the loop handles one event time t:
-//   release (implicit: a started GPU tool runs while T > t), immediate starts
-//   of cpu / gpu_now tools ready at t with the out-of-memory check, one FIFO
-//   queue admission, contention-scaled durations with k counting co-starters,
-//   ready times of tools whose predecessors have all started, next event.
+// gnm / gqm: tools on gpu_now / gpu_queue (internal labels; the rest run on
+// the CPU).  Per-tool state lives in four register arrays:
+//   Rn[i]  ready time of a waiting gpu_now tool (kInf otherwise)
+//   Rq[i]  ready time of a waiting gpu_queue tool (kInf otherwise)
+//   F[i]   finish time of a started GPU tool (0 before it starts)
+//   Fc[i]  finish time of a CPU tool (0 before its inputs are known)
+// A CPU tool starts the moment its inputs arrive and neither slows nor blocks
+// anything, so it is resolved as soon as all its predecessors have started;
+// the ascending sweep over topological labels resolves chains of CPU tools
+// in one pass.  Pass 0 only resolves the sources; every later pass handles
+// one event time t:
+//   A. GPU tools running at t (F > t) plus gpu_now tools ready at t give the
+//      concurrency k and the VRAM in use (over the budget: out of memory);
+//      if no queued tool is running, the ready queued tool with the smallest
+//      (ready time, original number) is admitted when it fits;
+//   B. in label order: starters get F = t + dur[k], fixed for their life;
+//      tools whose predecessors have all started get their ready time
+//      r = max over u -> i of finish(u) (+ xfer_i across devices); and the
+//      next event is accumulated: gpu_now and gpu_queue ready times after t,
+//      plus GPU finishes when a ready queued tool is still waiting (only the
+//      queue's own finish when the queue is busy).
 template <int N>
 __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict__ tab,
-                                             const uint32_t* __restrict__ s_dur,
-                                             uint32_t levels, uint32_t budget,
-                                             MaskT<N> gnm, MaskT<N> gqm) {
+                                                      const uint32_t* __restrict__ lds,
+                                                      uint32_t levels, uint32_t budget,
+                                                      MaskT<N> gnm, MaskT<N> gqm) {
   using M = MaskT<N>;
   const M ALL = all_tools<N>();
   const M gpum = gnm | gqm;
-  if (gpum & load_mask<N>(tab, kHdrBigLo)) return kInf;  // footprint > budget
-  const M src = load_mask<N>(tab, kHdrSrcLo);
+  if (gpum & load_mask<N>(Tab{tab}, kHdrBigLo)) return kInf;  // footprint > budget
+  const uint32_t* s_dur = lds;
+  const uint32_t* s_mem = lds + lds_mem_off<N>();
+  const uint32_t* s_pos = lds + lds_pos_off<N>();
 
-  uint32_t T[N];
+  uint32_t Rn[N], Rq[N], F[N], Fc[N];
 #pragma unroll
-  for (int v = 0; v < N; ++v) T[v] = bit<N>(src, v) ? 0u : kInf;
-
-  M started = 0;
+  for (int i = 0; i < N; ++i) {
+    Rn[i] = kInf;
+    Rq[i] = kInf;
+    F[i] = 0;
+    Fc[i] = 0;
+  }
+  M started = 0;   // started GPU tools and resolved CPU tools
+  M resolved = 0;  // tools whose ready time is known
   uint32_t t = 0;
-  uint32_t qfin = 0;  // finish time of the running queued tool (0: none)
+  uint32_t qfin = 0;     // finish of the running queued tool (0: none)
+  uint32_t minq = kInf;  // earliest ready time of a waiting queued tool
   uint32_t result = kInf;
 
-  for (int pass = 0; pass < 2 * N + 2; ++pass) {
-    // GPU tools still running at t, and the VRAM they hold.
-    const M sg = started & gpum;
+  for (int pass = 0; pass < 2 * N + 3; ++pass) {
+    const Tab tp = fresh(tab);
+    // A. concurrency and VRAM at t, after releases and immediate starts
     uint32_t in_use = 0, k = 0;
 #pragma unroll
-    for (int v = 0; v < N; ++v) {
-      if (bit<N>(sg, v) && T[v] > t) {
-        in_use += tab[kHdrWords + kToolWords * v + kToolMem];
-        k += 1;
-      }
-    }
-    // Immediate starts: waiting cpu / gpu_now tools whose ready time is t.
-    const M cand = ~started & ~gqm & ALL;
-    M st = 0;
-#pragma unroll
-    for (int v = 0; v < N; ++v)
-      if (bit<N>(cand, v) && T[v] == t) st |= M(1) << v;
-    const M stgn = st & gnm;
-#pragma unroll
-    for (int v = 0; v < N; ++v) {
-      if (bit<N>(stgn, v)) {
-        in_use += tab[kHdrWords + kToolWords * v + kToolMem];
-        k += 1;
-      }
+    for (int i = 0; i < N; ++i) {
+      const bool on = (F[i] > t) | (Rn[i] == t);
+      in_use += on ? tp[kHdrWords + kToolWords * i + kToolMem] : 0u;
+      k += on ? 1u : 0u;
     }
     if (in_use > budget) break;  // out of memory: infeasible
-
-    // Serialized queue: admit the ready queued tool with the smallest
-    // (ready time, index) if nothing queued is running and it fits.
-    M admitted = 0;
-    if (qfin <= t) {
-      const M qw = ~started & gqm & ALL;
-      uint32_t hT = kInf, hmem = 0;
-      M hbit = 0;
+    uint32_t hsel = kInf;        // label of the queued tool admitted at t
+    uint32_t waiting = 0;        // ready queued tools left waiting
+    if (minq <= t) {
+      if (qfin <= t) {
+        uint32_t hR = kInf;
 #pragma unroll
-      for (int v = 0; v < N; ++v) {
-        if (bit<N>(qw, v) && T[v] <= t && T[v] < hT) {
-          hT = T[v];
-          hbit = M(1) << v;
-          hmem = tab[kHdrWords + kToolWords * v + kToolMem];
+        for (int i = 0; i < N; ++i) {
+          const bool rd = Rq[i] <= t;
+          waiting += rd ? 1u : 0u;
+          hR = umin32(hR, rd ? Rq[i] : kInf);
+        }
+        uint32_t hO = kInf;  // FIFO ties go to the lowest original number
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+          hO = umin32(hO, Rq[i] == hR ? tp[kHdrWords + kToolWords * i + kToolOrig] : kInf);
+        const uint32_t lab = s_pos[hO];
+        if (s_mem[lab] <= budget - in_use) {
+          hsel = lab;
+          k += 1;
+          waiting -= 1;
+        }
+      } else {
+        waiting = 1;  // the queue is busy; its finish is the next chance
+      }
+    }
+    const uint32_t lev = umin32(umax32(k, 1u), levels) - 1u;
+
+    // B. starts, resolution, next event
+    const uint32_t t1 = t + 1u;
+    uint32_t tn = kInf, tq = kInf, tf = kInf;
+    minq = kInf;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const M bi = M(1) << i;
+      const bool adm = (hsel == uint32_t(i));
+      const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
+      if (Rn[i] == t || adm) {
+        const uint32_t d = s_dur[(uint32_t(i) * 2u + (adm ? 1u : 0u)) * levels + lev];
+        F[i] = t + d;
+        Rn[i] = kInf;
+        Rq[i] = kInf;
+        started |= bi;
+        if (adm) qfin = F[i];
+      } else if (((started & pm) | (resolved & bi)) == pm) {
+        const Tab rec = fresh(tab) + (kHdrWords + kToolWords * i);
+        uint32_t g = 0, c = 0;  // latest GPU / CPU predecessor finish
+        // Predecessors carry smaller labels; the mask test is wave-uniform.
+#pragma unroll
+        for (int u = 0; u < i; ++u) {
+          if ((pm >> u) & 1) {  // scalar branch: no vector work for non-edges
+            DEVMAP_KEEP_BRANCH();
+            g = umax32(g, F[u]);
+            c = umax32(c, Fc[u]);
+          }
+        }
+        const uint32_t xw = rec[kToolXfer];
+        const bool on_gpu = (gpum & bi) != 0;
+        const uint32_t r = on_gpu ? umax32(g, c ? c + xw : 0u) : umax32(c, g ? g + xw : 0u);
+        resolved |= bi;
+        if (!on_gpu) {
+          Fc[i] = r + rec[kToolCpu];
+          started |= bi;
+        } else if (gnm & bi) {
+          Rn[i] = r;
+        } else {
+          Rq[i] = r;
         }
       }
-      if (hbit != 0 && hmem <= budget - in_use) {
-        admitted = hbit;
-        k += 1;
-      }
+      tn = umin32(tn, Rn[i]);
+      minq = umin32(minq, Rq[i]);
+      tq = umin32(tq, Rq[i] - t1);  // wraps for ready times <= t
+      tf = umin32(tf, F[i] - t1);   // wraps for finished and unstarted tools
     }
-    st |= admitted;
-
-    // Durations of everything starting at t.
-    const uint32_t lev = umin32(umax32(k, 1u), levels) - 1u;
-#pragma unroll
-    for (int v = 0; v < N; ++v) {
-      if (bit<N>(st, v)) {
-        uint32_t d;
-        if (bit<N>(gpum, v))
-          d = s_dur[(uint32_t(v) * 2u + uint32_t(bit<N>(gqm, v))) * levels + lev];
-        else
-          d = tab[kHdrWords + kToolWords * v + kToolCpu];
-        T[v] = t + d;
-        if (bit<N>(admitted, v)) qfin = T[v];
-      }
-    }
-    started |= st;
     if (started == ALL) {
       uint32_t ms = 0;
 #pragma unroll
-      for (int v = 0; v < N; ++v) ms = umax32(ms, T[v]);
+      for (int i = 0; i < N; ++i) ms = umax32(ms, umax32(F[i], Fc[i]));
       result = ms;
       break;
     }
-
-    // Ready times of waiting tools whose predecessors have all started:
-    // r_w = max over u -> w of C_u (+ xfer_w when u and w sit on different
-    // devices).  Predecessor lists are wave-uniform; T[u] is read with a
-    // uniform register index.
-#pragma unroll
-    for (int w = 0; w < N; ++w) {
-      const uint32_t* rec = tab + kHdrWords + kToolWords * w;
-      const M pm = load_mask<N>(rec, kToolPredLo);
-      if (!bit<N>(started, w) && T[w] == kInf && (pm & ~started) == 0) {
-        const uint32_t np = rec[kToolNPred];
-        const uint32_t* pl = tab + kPredBase + rec[kToolPredOff];
-        const uint32_t xw = rec[kToolXfer];
-        const bool gw = bit<N>(gpum, w);
-        uint32_t r = 0;
-        for (uint32_t j = 0; j < np; ++j) {
-          const int u = DEVMAP_UNIFORM(int(pl[j]));
-          const uint32_t arrive = T[u] + ((bit<N>(gpum, u) != gw) ? xw : 0u);
-          r = umax32(r, arrive);
-        }
-        T[w] = r;
+    if (pass == 0) continue;  // sources resolved: now the events at t = 0
+    // Times stay below 2^31, so a difference that wrapped (a time <= t)
+    // is >= 2^31 and a genuine later time is below it.
+    if (tq < 0x80000000u) tn = umin32(tn, tq + t1);
+    if (waiting != 0) {
+      if (qfin > t) {
+        tn = umin32(tn, qfin);           // queue busy: wait for it
+      } else if (tf < 0x80000000u) {
+        tn = umin32(tn, tf + t1);        // blocked on VRAM: wait for a release
       }
     }
-
-    // Next event: the smallest ready or finish time after t.
-    uint32_t tn = kInf;
-#pragma unroll
-    for (int v = 0; v < N; ++v) tn = umin32(tn, T[v] > t ? T[v] : kInf);
     if (tn == kInf) break;  // a queued tool can never fit: infeasible
     t = tn;
   }
   return result;
 }
 
-// Decode tools lo_tool..N-1 of x (x = their base-3 digits, lowest first)
-// into mode masks.
+// Mode masks (internal labels) of tools lo_tool..N-1 of x: x holds their
+// base-3 digits, lowest first, and original tool v maps to label pos[v].
 template <int N>
-__host__ __device__ __forceinline__ void decode_digits(uint64_t x, int lo_tool, MaskT<N>& gn,
-                                              MaskT<N>& gq) {
+__host__ __device__ __forceinline__ void decode_digits(const uint32_t* __restrict__ tab,
+                                                      uint64_t x, int lo_tool, MaskT<N>& gn,
+                                                      MaskT<N>& gq) {
   using M = MaskT<N>;
   gn = 0;
   gq = 0;
@@ -199,16 +268,18 @@ __host__ __device__ __forceinline__ void decode_digits(uint64_t x, int lo_tool, 
     uint32_t y = uint32_t(x);
     for (int v = lo_tool; v < N; ++v) {
       const uint32_t q = y / 3u, d = y - 3u * q;
-      if (d == 1) gn |= M(1) << v;
-      if (d == 2) gq |= M(1) << v;
+      const M b = M(1) << tab[kPosBase + v];
+      if (d == 1) gn |= b;
+      if (d == 2) gq |= b;
       y = q;
     }
   } else {
     for (int v = lo_tool; v < N; ++v) {
       const uint64_t q = x / 3u;
       const uint32_t d = uint32_t(x - 3u * q);
-      if (d == 1) gn |= M(1) << v;
-      if (d == 2) gq |= M(1) << v;
+      const M b = M(1) << tab[kPosBase + v];
+      if (d == 1) gn |= b;
+      if (d == 2) gq |= b;
       x = q;
     }
   }
@@ -243,10 +314,14 @@ __device__ __forceinline__ void block_min(uint32_t& ms, uint64_t& x) {
 }
 
 template <int N>
-__device__ __forceinline__ void stage_durations(const uint32_t* tab, uint32_t* s_dur) {
+__device__ __forceinline__ void stage_tables(const uint32_t* tab, uint32_t* lds) {
   const uint32_t levels = tab[kHdrLevels];
   const uint32_t* dur = tab + tab[kHdrDurOff];
-  for (uint32_t i = threadIdx.x; i < uint32_t(N) * 2u * levels; i += blockDim.x) s_dur[i] = dur[i];
+  for (uint32_t i = threadIdx.x; i < uint32_t(N) * 2u * levels; i += blockDim.x) lds[i] = dur[i];
+  for (uint32_t i = threadIdx.x; i < uint32_t(N); i += blockDim.x) {
+    lds[lds_mem_off<N>() + i] = tab[kHdrWords + kToolWords * i + kToolMem];
+    lds[lds_pos_off<N>() + i] = tab[kPosBase + i];
+  }
   __syncthreads();
 }
 
@@ -258,7 +333,7 @@ __device__ __forceinline__ void stage_durations(const uint32_t* tab, uint32_t* s
 template <int N>
 __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
                                                      const uint32_t* __restrict__ tab,
-                                                     const uint32_t* __restrict__ s_dur,
+                                                     const uint32_t* __restrict__ lds,
                                                      uint64_t item, uint32_t lane,
                                                      uint32_t& best_ms, uint64_t& best_x) {
   using M = MaskT<N>;
@@ -269,7 +344,7 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
   const uint32_t J = a.inner_digits;
   const uint64_t o = a.outer_lo + rel;
   M ogn, ogq;
-  decode_digits<N>(o, int(J), ogn, ogq);  // o's digits are tools J..N-1
+  decode_digits<N>(tab, o, int(J), ogn, ogq);  // o's digits are tools J..N-1
   const uint64_t base = o * a.inner_count;
   // Inner index bounds of this lane inside [lo, hi).
   const uint64_t ilo64 = a.lo > base ? a.lo - base : 0;
@@ -279,15 +354,15 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
   M ign = 0, igq = 0;  // inner modes: the same in every lane of the wave
   for (uint32_t i = 0; i < a.inner_count; ++i) {
     if (i >= ilo && i < ihi) {
-      const uint32_t ms = evaluate<N>(tab, s_dur, levels, budget, ogn | ign, ogq | igq);
+      const uint32_t ms = evaluate<N>(tab, lds, levels, budget, ogn | ign, ogq | igq);
       if (ms < best_ms) {
         best_ms = ms;
         best_x = base + i;
       }
     }
-    // odometer step on the inner digits
-    M b = 1;
-    for (uint32_t j = 0; j < J; ++j, b <<= 1) {
+    // odometer step on the inner digits (original tools 0..J-1)
+    for (uint32_t j = 0; j < J; ++j) {
+      const M b = M(1) << tab[kPosBase + j];
       if (igq & b) {
         igq &= ~b;
         continue;
@@ -309,16 +384,16 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // block's minimum goes to partials[b].
 template <int N>
 __global__ __launch_bounds__(kBlock) void search_kernel(SearchArgs a) {
-  __shared__ uint32_t s_dur[N * 2 * (N < kMaxLevels ? N : kMaxLevels)];
+  __shared__ uint32_t s_lds[lds_words<N>()];
   const uint32_t table = blockIdx.x / a.blocks_per_table;
   const uint32_t bb = blockIdx.x - table * a.blocks_per_table;
   const uint32_t* tab = a.tables + size_t(table) * a.table_stride;
-  stage_durations<N>(tab, s_dur);
+  stage_tables<N>(tab, s_lds);
 
   uint32_t best_ms = kInf;
   uint64_t best_x = ~0ull;
   for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-    lane_search<N>(a, tab, s_dur, item, threadIdx.x, best_ms, best_x);
+    lane_search<N>(a, tab, s_lds, item, threadIdx.x, best_ms, best_x);
 
   block_min(best_ms, best_x);
   if (threadIdx.x == 0) {
@@ -337,8 +412,8 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
                                                       int64_t n, uint64_t n_mappings,
                                                       int64_t* __restrict__ out) {
   using M = MaskT<N>;
-  __shared__ uint32_t s_dur[N * 2 * (N < kMaxLevels ? N : kMaxLevels)];
-  stage_durations<N>(tab, s_dur);
+  __shared__ uint32_t s_lds[lds_words<N>()];
+  stage_tables<N>(tab, s_lds);
   const uint32_t levels = tab[kHdrLevels];
   const uint32_t budget = tab[kHdrBudget];
   for (int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x; i < n;
@@ -347,8 +422,8 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
     int64_t r = INT64_MAX;
     if (x < n_mappings) {
       M gn, gq;
-      decode_digits<N>(x, 0, gn, gq);
-      const uint32_t ms = evaluate<N>(tab, s_dur, levels, budget, gn, gq);
+      decode_digits<N>(tab, x, 0, gn, gq);
+      const uint32_t ms = evaluate<N>(tab, s_lds, levels, budget, gn, gq);
       if (ms != kInf) r = int64_t(ms);
     }
     out[i] = r;

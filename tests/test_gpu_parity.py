@@ -90,10 +90,10 @@ def test_out_of_range_indices_are_infeasible(torch_cuda, O):
     assert list(got[:3]) == [INF64] * 3 and got[3] == Q.eval_index(7)
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(32))
 def test_random_dags_every_index(torch_cuda, O, seed):
     n = 1 + seed % 8
-    shape = ["random", "chain", "fanout"][seed % 3]
+    shape = ["random", "chain", "fanout", "permuted"][seed % 4]
     inst = synth.random_instance(2000 + seed, n, shape, levels=1 + seed % 5,
                                  tight=(seed % 2 == 0), small_values=(seed % 4 == 1))
     P, Q = both(inst, O)

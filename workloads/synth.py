@@ -290,7 +290,9 @@ def random_instance(seed: int, n: int, shape: str = "random", levels: int = 4,
                     tight: bool = False, small_values: bool = False) -> Dict:
     """A random instance with n tools.
 
-    shape: "chain", "fanout", "random" (edge u->v, u<v, probability 0.3).
+    shape: "chain", "fanout", "random" (edge u->v, u<v, probability 0.3),
+    "permuted" (the random shape with tool numbers shuffled, so that tool
+    numbers are not a topological order).
     tight: budget a quarter of the summed footprint (forces queueing).
     small_values: latencies in 1..60 so tick-by-tick simulation is cheap.
     """
@@ -313,6 +315,12 @@ def random_instance(seed: int, n: int, shape: str = "random", levels: int = 4,
     else:
         edges = [[u, v] for u in range(n) for v in range(u + 1, n)
                  if rng.uniform() < 0.3]
+        if shape == "permuted":
+            perm = list(range(n))
+            for i in range(n - 1, 0, -1):
+                j = rng.below(i + 1)
+                perm[i], perm[j] = perm[j], perm[i]
+            edges = [[perm[u], perm[v]] for u, v in edges]
     total = sum(t[4] for t in tools)
     budget = total // 4 if tight else max(total // 2, max(t[4] for t in tools))
     table = [65536]
