@@ -19,6 +19,7 @@ struct sched_problem {
   std::vector<sched_tool> tools;
   std::vector<std::vector<int32_t>> preds;  // ascending, deduplicated
   std::vector<int32_t> order;               // order[i]: original tool with internal label i
+  std::vector<int32_t> late;                // tools from the deepest in the DAG to the shallowest
   std::vector<uint32_t> contention;         // F[k-1]
   int64_t budget = 0;
   uint64_t n_mappings = 0;
@@ -114,6 +115,12 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
     out[kPosBase + v] = uint32_t(i);
     if (tl.mem_mib > budget) big |= 1ull << i;
   }
+  for (int v = 0; v < n; ++v) {  // index order: digit position v is tool v
+    out[kEnumLabBase + v] = uint32_t(label[v]);
+    const uint64_t w = pow3(v);
+    out[kEnumWeightBase + 2 * v] = uint32_t(w);
+    out[kEnumWeightBase + 2 * v + 1] = uint32_t(w >> 32);
+  }
   out[kHdrN] = uint32_t(n);
   out[kHdrLevels] = uint32_t(levels);
   out[kHdrBudget] = uint32_t(budget);
@@ -145,6 +152,28 @@ void plan_search(int n, uint64_t lo, uint64_t hi, uint32_t n_tables, SearchArgs&
   const uint64_t cap = std::max<uint64_t>(1, kMaxBlocks / n_tables);
   a.blocks_per_table = uint32_t(std::min<uint64_t>(a.items_per_table, cap));
   a.n_tables = n_tables;
+  a.full_range = (lo == 0 && hi == pow3(n)) ? 1u : 0u;
+}
+
+// Enumeration order of a full-range search: the four tools deepest in the
+// DAG take the positions right above the J inner digits, so that the lanes of
+// a wave (consecutive outer combinations) differ in tools that act late in
+// every schedule and step through their passes together; the other tools
+// follow from deepest to shallowest.  Any order visits every mapping once.
+void set_late_enumeration(const sched_problem& p, int J, uint32_t* table) {
+  const int n = p.n;
+  std::vector<int32_t> seq;
+  const int lanes = std::min(4, n - J);
+  for (int k = 0; k < J; ++k) seq.push_back(p.late[lanes + k]);
+  for (int k = 0; k < lanes; ++k) seq.push_back(p.late[k]);
+  for (int k = lanes + J; k < n; ++k) seq.push_back(p.late[k]);
+  for (int pos = 0; pos < n; ++pos) {
+    const int v = seq[pos];
+    table[kEnumLabBase + pos] = table[kPosBase + v];
+    const uint64_t w = pow3(v);
+    table[kEnumWeightBase + 2 * pos] = uint32_t(w);
+    table[kEnumWeightBase + 2 * pos + 1] = uint32_t(w >> 32);
+  }
 }
 
 size_t partial_capacity(uint64_t n_tables) {
@@ -243,6 +272,27 @@ int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_e
       delete p;
       return SCHED_E_CYCLE;
     }
+    // Depth of every tool (longest chain from a source, in tools) and its
+    // number of ancestors, in topological order; deepest first, ties to
+    // more ancestors, then to the lower tool number.
+    std::vector<int32_t> depth(n_tools, 1);
+    std::vector<std::vector<char>> anc(n_tools, std::vector<char>(n_tools, 0));
+    for (int32_t v : p->order)
+      for (int32_t u : p->preds[v]) {
+        depth[v] = std::max(depth[v], depth[u] + 1);
+        anc[v][u] = 1;
+        for (int32_t w = 0; w < n_tools; ++w)
+          if (anc[u][w]) anc[v][w] = 1;
+      }
+    std::vector<int32_t> n_anc(n_tools, 0);
+    for (int32_t v = 0; v < n_tools; ++v)
+      for (int32_t w = 0; w < n_tools; ++w) n_anc[v] += anc[v][w];
+    p->late.resize(n_tools);
+    std::iota(p->late.begin(), p->late.end(), 0);
+    std::stable_sort(p->late.begin(), p->late.end(), [&](int32_t a, int32_t b) {
+      if (depth[a] != depth[b]) return depth[a] > depth[b];
+      return n_anc[a] > n_anc[b];
+    });
     p->n_mappings = pow3(n_tools);
     p->table_words = table_words(n_tools, total, std::min<int>(n_levels, n_tools));
     p->table.assign(p->table_words, 0u);
@@ -309,7 +359,14 @@ int sched_bruteforce_argmin(const sched_problem* p, uint64_t lo, uint64_t hi, vo
   a.partials = reinterpret_cast<Partial*>(ws + L.partials);
   DevResult* d_res = reinterpret_cast<DevResult*>(ws + L.results);
 
-  HIP_TRY(hipMemcpyAsync(ws + L.tables, p->table.data(), size_t(p->table_words) * 4,
+  std::vector<uint32_t> table;
+  try {
+    table = p->table;
+  } catch (const std::bad_alloc&) {
+    return SCHED_E_NOMEM;
+  }
+  if (a.full_range) set_late_enumeration(*p, int(a.inner_digits), table.data());
+  HIP_TRY(hipMemcpyAsync(ws + L.tables, table.data(), size_t(p->table_words) * 4,
                          hipMemcpyHostToDevice, s));
   HIP_TRY(launch_search(p->n, a, s));
   HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, 1, d_res, s));
@@ -361,11 +418,33 @@ int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
   } catch (const std::bad_alloc&) {
     return SCHED_E_NOMEM;
   }
-  for (size_t i = 0; i < R; ++i) {
-    const int32_t r = order[i];
-    const sched_problem& p = *problems[replica_problem[r]];
-    rc = build_table(p, replica_lat + lat_off[r], host_tables.data() + i * max_stride);
-    if (rc != SCHED_OK) return rc;
+  // Per group of equal tool count: the search plan, then the tables.
+  struct Group {
+    size_t first, last;
+    SearchArgs a;
+  };
+  std::vector<Group> groups;
+  for (size_t first = 0; first < R;) {
+    const int n = problems[replica_problem[order[first]]]->n;
+    size_t last = first;
+    while (last < R && problems[replica_problem[order[last]]]->n == n) ++last;
+    Group g{first, last, SearchArgs{}};
+    plan_search(n, 0, pow3(n), uint32_t(last - first), g.a);
+    // The block cap is shared by the whole batch so partials stay bounded.
+    const uint64_t cap = std::max<uint64_t>(1, kMaxBlocks / R);
+    g.a.blocks_per_table = uint32_t(std::min<uint64_t>(g.a.items_per_table, cap));
+    groups.push_back(g);
+    first = last;
+  }
+  for (const Group& g : groups) {
+    for (size_t i = g.first; i < g.last; ++i) {
+      const int32_t r = order[i];
+      const sched_problem& p = *problems[replica_problem[r]];
+      uint32_t* tb = host_tables.data() + i * max_stride;
+      rc = build_table(p, replica_lat + lat_off[r], tb);
+      if (rc != SCHED_OK) return rc;
+      set_late_enumeration(p, int(g.a.inner_digits), tb);
+    }
   }
 
   hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
@@ -375,24 +454,17 @@ int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
   DevResult* d_res = reinterpret_cast<DevResult*>(ws + L.results);
   HIP_TRY(hipMemcpyAsync(ws + L.tables, host_tables.data(), R * max_stride * 4,
                          hipMemcpyHostToDevice, s));
-  size_t first = 0, partial_cursor = 0;
-  while (first < R) {
-    const int n = problems[replica_problem[order[first]]]->n;
-    size_t last = first;
-    while (last < R && problems[replica_problem[order[last]]]->n == n) ++last;
-    const uint32_t count = uint32_t(last - first);
-    SearchArgs a{};
-    // The block cap is shared by the whole batch so partials stay bounded.
-    plan_search(n, 0, pow3(n), count, a);
-    const uint64_t cap = std::max<uint64_t>(1, kMaxBlocks / R);
-    a.blocks_per_table = uint32_t(std::min<uint64_t>(a.items_per_table, cap));
-    a.tables = d_tables + first * max_stride;
+  size_t partial_cursor = 0;
+  for (Group& g : groups) {
+    const int n = problems[replica_problem[order[g.first]]]->n;
+    const uint32_t count = uint32_t(g.last - g.first);
+    SearchArgs& a = g.a;
+    a.tables = d_tables + g.first * max_stride;
     a.table_stride = uint32_t(max_stride);
     a.partials = d_partials + partial_cursor;
     HIP_TRY(launch_search(n, a, s));
-    HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, count, d_res + first, s));
+    HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, count, d_res + g.first, s));
     partial_cursor += size_t(count) * a.blocks_per_table;
-    first = last;
   }
   HIP_TRY(hipMemcpyAsync(host_res.data(), d_res, R * sizeof(DevResult), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));

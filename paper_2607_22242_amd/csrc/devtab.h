@@ -47,8 +47,14 @@ enum : uint32_t {
 
 // pos[v]: internal label of original tool v.
 constexpr uint32_t kPosBase = kHdrWords + kToolWords * kMaxTools;  // 336
+// Enumeration order of a search: digit position p of the enumeration holds
+// the mode of the tool with internal label elab[p], whose weight in the
+// mapping index is ew[p] = 3^(original number) (two words, low first).
+// Positions 0..J-1 are the inner digits, J.. the outer ones.
+constexpr uint32_t kEnumLabBase = kPosBase + kMaxTools;         // 376
+constexpr uint32_t kEnumWeightBase = kEnumLabBase + kMaxTools;  // 416
 // Predecessor lists (internal labels), then the duration table.
-constexpr uint32_t kPredBase = kPosBase + kMaxTools;  // 376
+constexpr uint32_t kPredBase = kEnumWeightBase + 2 * kMaxTools;  // 496
 
 // Duration table: dur[(i * 2 + q) * levels + (level - 1)] for internal label
 // i, q = 0 for gpu_now (base gpu_us), q = 1 for gpu_queue (gpu_us + load_us).
@@ -72,10 +78,11 @@ struct SearchArgs {
   uint64_t n_outer;           // outer combinations covering [lo, hi)
   uint32_t table_stride;
   uint32_t n_tables;
-  uint32_t inner_digits;      // J: tools 0..J-1 are enumerated per lane
+  uint32_t inner_digits;      // J: enumeration positions 0..J-1 are walked per lane
   uint32_t inner_count;       // 3^J
   uint64_t items_per_table;   // ceil(n_outer / kBlock)
   uint32_t blocks_per_table;
+  uint32_t full_range;        // 1: [lo, hi) = [0, 3^N), any enumeration order
 };
 
 struct DevResult {

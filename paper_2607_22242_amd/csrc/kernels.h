@@ -96,20 +96,25 @@ constexpr uint32_t lds_pos_off() { return lds_mem_off<N>() + uint32_t(N); }
 template <int N>
 constexpr uint32_t lds_words() { return lds_pos_off<N>() + uint32_t(N); }
 
-// Makespan of one mapping under the schedule model, or kInf if infeasible.
+// Event-driven schedule of one mapping (the schedule model in full), advanced
+// one event time per call of step().
 //
 // gnm / gqm: tools on gpu_now / gpu_queue (internal labels; the rest run on
-// the CPU).  Per-tool state lives in four register arrays:
-//   Rn[i]  ready time of a waiting gpu_now tool (kInf otherwise)
-//   Rq[i]  ready time of a waiting gpu_queue tool (kInf otherwise)
-//   F[i]   finish time of a started GPU tool (0 before it starts)
-//   Fc[i]  finish time of a CPU tool (0 before its inputs are known)
+// the CPU).  Per-tool state lives in two register arrays; times stay below
+// 2^31 - 1 (a creation-time guard), which frees the top bit as a tag:
+//   R[i]  ready time of a waiting tool: r for gpu_now, r | 2^31 for
+//         gpu_queue; kNoReady (2^31 - 1) when not waiting
+//   F[i]  finish time of a started tool: f for a GPU tool, f | 2^31 for a
+//         CPU tool; 0 before it starts
+// Unsigned differences then answer every question with one compare: a GPU
+// tool runs at t iff F - (t+1) < 2^31 - (t+1); a queued tool is ready iff
+// R - 2^31 <= t; and so on.
 // A CPU tool starts the moment its inputs arrive and neither slows nor blocks
 // anything, so it is resolved as soon as all its predecessors have started;
 // the ascending sweep over topological labels resolves chains of CPU tools
 // in one pass.  Pass 0 only resolves the sources; every later pass handles
 // one event time t:
-//   A. GPU tools running at t (F > t) plus gpu_now tools ready at t give the
+//   A. GPU tools running at t plus gpu_now tools ready at t give the
 //      concurrency k and the VRAM in use (over the budget: out of memory);
 //      if no queued tool is running, the ready queued tool with the smallest
 //      (ready time, original number) is admitted when it fits;
@@ -119,60 +124,82 @@ constexpr uint32_t lds_words() { return lds_pos_off<N>() + uint32_t(N); }
 //      next event is accumulated: gpu_now and gpu_queue ready times after t,
 //      plus GPU finishes when a ready queued tool is still waiting (only the
 //      queue's own finish when the queue is busy).
+// A mapping needs at most 2N+1 passes: every pass after the first moves t to
+// a ready or finish time, and each tool has one of each.
+constexpr uint32_t kTag = 0x80000000u;
+constexpr uint32_t kNoReady = 0x7FFFFFFFu;
+
 template <int N>
-__host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict__ tab,
-                                                      const uint32_t* __restrict__ lds,
-                                                      uint32_t levels, uint32_t budget,
-                                                      MaskT<N> gnm, MaskT<N> gqm) {
+struct Sim {
   using M = MaskT<N>;
-  const M ALL = all_tools<N>();
-  const M gpum = gnm | gqm;
-  if (gpum & load_mask<N>(Tab{tab}, kHdrBigLo)) return kInf;  // footprint > budget
-  const uint32_t* s_dur = lds;
-  const uint32_t* s_mem = lds + lds_mem_off<N>();
-  const uint32_t* s_pos = lds + lds_pos_off<N>();
+  uint32_t R[N], F[N];
+  M gnm, gqm;
+  M started;   // started GPU tools and resolved CPU tools
+  M resolved;  // tools whose ready time is known
+  uint32_t t;
+  uint32_t qfin;  // finish of the running queued tool (0: none)
+  uint32_t minq;  // earliest ready time of a waiting queued tool (>= 2^31: none)
+  int pass;       // passes done; -1: statically infeasible
 
-  uint32_t Rn[N], Rq[N], F[N], Fc[N];
+  __host__ __device__ __forceinline__ void init(const uint32_t* __restrict__ tab, M gn, M gq) {
+    gnm = gn;
+    gqm = gq;
 #pragma unroll
-  for (int i = 0; i < N; ++i) {
-    Rn[i] = kInf;
-    Rq[i] = kInf;
-    F[i] = 0;
-    Fc[i] = 0;
+    for (int i = 0; i < N; ++i) {
+      R[i] = kNoReady;
+      F[i] = 0;
+    }
+    started = 0;
+    resolved = 0;
+    t = 0;
+    qfin = 0;
+    minq = kInf;
+    // a GPU mode whose footprint exceeds the budget never fits
+    pass = ((gn | gq) & load_mask<N>(Tab{tab}, kHdrBigLo)) ? -1 : 0;
   }
-  M started = 0;   // started GPU tools and resolved CPU tools
-  M resolved = 0;  // tools whose ready time is known
-  uint32_t t = 0;
-  uint32_t qfin = 0;     // finish of the running queued tool (0: none)
-  uint32_t minq = kInf;  // earliest ready time of a waiting queued tool
-  uint32_t result = kInf;
 
-  for (int pass = 0; pass < 2 * N + 3; ++pass) {
+  // One pass.  Returns true when the mapping is settled; ms then holds its
+  // makespan, or kInf if it is infeasible.
+  __host__ __device__ __forceinline__ bool step(const uint32_t* __restrict__ tab,
+                                                const uint32_t* __restrict__ lds,
+                                                uint32_t levels, uint32_t budget,
+                                                uint32_t& ms) {
+    ms = kInf;
+    if (pass < 0 || pass > 2 * N + 1) return true;
+    const M ALL = all_tools<N>();
+    const M gpum = gnm | gqm;
+    const uint32_t* s_dur = lds;
+    const uint32_t* s_mem = lds + lds_mem_off<N>();
+    const uint32_t* s_pos = lds + lds_pos_off<N>();
     const Tab tp = fresh(tab);
+    const uint32_t t1 = t + 1u;
+    const uint32_t lim = kTag - t1;  // F - t1 < lim: a GPU tool running at t
+
     // A. concurrency and VRAM at t, after releases and immediate starts
     uint32_t in_use = 0, k = 0;
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const bool on = (F[i] > t) | (Rn[i] == t);
+      const bool on = (F[i] - t1 < lim) | (R[i] == t);
       in_use += on ? tp[kHdrWords + kToolWords * i + kToolMem] : 0u;
       k += on ? 1u : 0u;
     }
-    if (in_use > budget) break;  // out of memory: infeasible
-    uint32_t hsel = kInf;        // label of the queued tool admitted at t
-    uint32_t waiting = 0;        // ready queued tools left waiting
+    if (in_use > budget) return true;  // out of memory: infeasible
+    uint32_t hsel = kInf;              // label of the queued tool admitted at t
+    uint32_t waiting = 0;              // ready queued tools left waiting
     if (minq <= t) {
       if (qfin <= t) {
         uint32_t hR = kInf;
 #pragma unroll
         for (int i = 0; i < N; ++i) {
-          const bool rd = Rq[i] <= t;
+          const uint32_t rq = R[i] - kTag;  // queued: its ready time; others wrap high
+          const bool rd = rq <= t;
           waiting += rd ? 1u : 0u;
-          hR = umin32(hR, rd ? Rq[i] : kInf);
+          hR = umin32(hR, rd ? rq : kInf);
         }
         uint32_t hO = kInf;  // FIFO ties go to the lowest original number
 #pragma unroll
         for (int i = 0; i < N; ++i)
-          hO = umin32(hO, Rq[i] == hR ? tp[kHdrWords + kToolWords * i + kToolOrig] : kInf);
+          hO = umin32(hO, R[i] - kTag == hR ? tp[kHdrWords + kToolWords * i + kToolOrig] : kInf);
         const uint32_t lab = s_pos[hO];
         if (s_mem[lab] <= budget - in_use) {
           hsel = lab;
@@ -186,7 +213,6 @@ __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict
     const uint32_t lev = umin32(umax32(k, 1u), levels) - 1u;
 
     // B. starts, resolution, next event
-    const uint32_t t1 = t + 1u;
     uint32_t tn = kInf, tq = kInf, tf = kInf;
     minq = kInf;
 #pragma unroll
@@ -194,65 +220,81 @@ __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict
       const M bi = M(1) << i;
       const bool adm = (hsel == uint32_t(i));
       const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
-      if (Rn[i] == t || adm) {
+      if (R[i] == t || adm) {
         const uint32_t d = s_dur[(uint32_t(i) * 2u + (adm ? 1u : 0u)) * levels + lev];
         F[i] = t + d;
-        Rn[i] = kInf;
-        Rq[i] = kInf;
+        R[i] = kNoReady;
         started |= bi;
         if (adm) qfin = F[i];
       } else if (((started & pm) | (resolved & bi)) == pm) {
         const Tab rec = fresh(tab) + (kHdrWords + kToolWords * i);
-        uint32_t g = 0, c = 0;  // latest GPU / CPU predecessor finish
+        uint32_t g = 0, c = 0;  // latest GPU finish; latest finish overall
         // Predecessors carry smaller labels; the mask test is wave-uniform.
 #pragma unroll
         for (int u = 0; u < i; ++u) {
           if ((pm >> u) & 1) {  // scalar branch: no vector work for non-edges
             DEVMAP_KEEP_BRANCH();
-            g = umax32(g, F[u]);
-            c = umax32(c, Fc[u]);
+            const uint32_t f = F[u];
+            g = umax32(g, f < kTag ? f : 0u);
+            c = umax32(c, f);  // CPU finishes carry the tag, so they dominate
           }
         }
+        c = c >= kTag ? c - kTag : 0u;  // latest CPU finish (0: none)
         const uint32_t xw = rec[kToolXfer];
         const bool on_gpu = (gpum & bi) != 0;
         const uint32_t r = on_gpu ? umax32(g, c ? c + xw : 0u) : umax32(c, g ? g + xw : 0u);
         resolved |= bi;
         if (!on_gpu) {
-          Fc[i] = r + rec[kToolCpu];
+          F[i] = (r + rec[kToolCpu]) | kTag;
           started |= bi;
         } else if (gnm & bi) {
-          Rn[i] = r;
+          R[i] = r;
         } else {
-          Rq[i] = r;
+          R[i] = r | kTag;
         }
       }
-      tn = umin32(tn, Rn[i]);
-      minq = umin32(minq, Rq[i]);
-      tq = umin32(tq, Rq[i] - t1);  // wraps for ready times <= t
-      tf = umin32(tf, F[i] - t1);   // wraps for finished and unstarted tools
+      tn = umin32(tn, R[i]);             // gpu_now ready times (queued ones are tagged high)
+      const uint32_t rq = R[i] - kTag;  // queued ready time; others wrap high
+      minq = umin32(minq, rq);
+      tq = umin32(tq, rq - t1);          // wraps for ready times <= t
+      tf = umin32(tf, F[i] - t1);        // below lim only for GPU tools running after t
     }
+    ++pass;
     if (started == ALL) {
-      uint32_t ms = 0;
+      uint32_t m = 0;
 #pragma unroll
-      for (int i = 0; i < N; ++i) ms = umax32(ms, umax32(F[i], Fc[i]));
-      result = ms;
-      break;
+      for (int i = 0; i < N; ++i) m = umax32(m, F[i] & ~kTag);
+      ms = m;
+      return true;
     }
-    if (pass == 0) continue;  // sources resolved: now the events at t = 0
-    // Times stay below 2^31, so a difference that wrapped (a time <= t)
-    // is >= 2^31 and a genuine later time is below it.
-    if (tq < 0x80000000u) tn = umin32(tn, tq + t1);
+    if (pass == 1) return false;  // sources resolved: now the events at t = 0
+    if (tn >= kNoReady) tn = kInf;
+    if (tq < kTag) tn = umin32(tn, tq + t1);
     if (waiting != 0) {
       if (qfin > t) {
-        tn = umin32(tn, qfin);           // queue busy: wait for it
-      } else if (tf < 0x80000000u) {
-        tn = umin32(tn, tf + t1);        // blocked on VRAM: wait for a release
+        tn = umin32(tn, qfin);     // queue busy: wait for it
+      } else if (tf < lim) {
+        tn = umin32(tn, tf + t1);  // blocked on VRAM: wait for a release
       }
     }
-    if (tn == kInf) break;  // a queued tool can never fit: infeasible
+    if (tn == kInf) return true;  // a queued tool can never fit: infeasible
     t = tn;
+    return false;
   }
-  return result;
+};
+
+// Makespan of one mapping, or kInf if it is infeasible.
+template <int N>
+__host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict__ tab,
+                                                      const uint32_t* __restrict__ lds,
+                                                      uint32_t levels, uint32_t budget,
+                                                      MaskT<N> gnm, MaskT<N> gqm) {
+  Sim<N> sim;
+  sim.init(tab, gnm, gqm);
+  uint32_t ms = kInf;
+  while (!sim.step(tab, lds, levels, budget, ms)) {
+  }
+  return ms;
 }
 
 // Mode masks (internal labels) of tools lo_tool..N-1 of x: x holds their
@@ -325,18 +367,61 @@ __device__ __forceinline__ void stage_tables(const uint32_t* tab, uint32_t* lds)
   __syncthreads();
 }
 
-// One lane's share of one work item: outer combination
-// outer_lo + item * kBlock + lane (the modes of tools J..N-1), combined with
-// every inner combination (tools 0..J-1) whose index lies in [lo, hi).
-// Updates the lane's running (makespan, index) minimum; indices are visited
-// in increasing order, so a strict comparison keeps the lowest index.
+// Mode masks and index weight of enumeration positions [p0, p1) holding
+// the base-3 digits of y (lowest first).
 template <int N>
+__host__ __device__ __forceinline__ void decode_positions(const uint32_t* __restrict__ tab,
+                                                         uint64_t y, uint32_t p0, uint32_t p1,
+                                                         MaskT<N>& gn, MaskT<N>& gq,
+                                                         uint64_t& x) {
+  using M = MaskT<N>;
+  gn = 0;
+  gq = 0;
+  x = 0;
+  for (uint32_t p = p0; p < p1; ++p) {
+    const uint64_t q = y / 3u;
+    const uint32_t d = uint32_t(y - 3u * q);
+    const M b = M(1) << tab[kEnumLabBase + p];
+    const uint64_t w = uint64_t(tab[kEnumWeightBase + 2 * p]) |
+                       (uint64_t(tab[kEnumWeightBase + 2 * p + 1]) << 32);
+    if (d == 1) {
+      gn |= b;
+      x += w;
+    }
+    if (d == 2) {
+      gq |= b;
+      x += 2 * w;
+    }
+    y = q;
+  }
+}
+
+// Waves per SIMD the search kernel is compiled for (the register budget).
+#ifndef DEVMAP_SEARCH_WAVES
+#define DEVMAP_SEARCH_WAVES 6
+#endif
+
+// Index arithmetic: 3^20 < 2^32, so up to 20 tools an index fits 32 bits.
+template <int N>
+using IdxT = typename std::conditional<(N <= 20), uint32_t, uint64_t>::type;
+
+// One lane's share of one work item: outer combination
+// outer_lo + item * kBlock + lane (the digits of enumeration positions J..N-1),
+// combined with every inner combination (positions 0..J-1) in range.  All
+// lanes of a wave start their mappings together and step them pass by pass,
+// which keeps the per-tool branches of a pass coherent across the wave.
+// FULL: the whole index range in the enumeration order of the table, whose
+// index need not grow along the walk, so the running minimum compares
+// (makespan, index) in full.  Otherwise: index order, o * 3^J + i, clipped to
+// [lo, hi); indices grow, so a strict comparison keeps the lowest index.
+template <int N, bool FULL>
 __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
                                                      const uint32_t* __restrict__ tab,
                                                      const uint32_t* __restrict__ lds,
                                                      uint64_t item, uint32_t lane,
                                                      uint32_t& best_ms, uint64_t& best_x) {
   using M = MaskT<N>;
+  using I = IdxT<N>;
   const uint64_t rel = item * kBlock + lane;
   if (rel >= a.n_outer) return;
   const uint32_t levels = tab[kHdrLevels];
@@ -344,29 +429,50 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
   const uint32_t J = a.inner_digits;
   const uint64_t o = a.outer_lo + rel;
   M ogn, ogq;
-  decode_digits<N>(tab, o, int(J), ogn, ogq);  // o's digits are tools J..N-1
-  const uint64_t base = o * a.inner_count;
-  // Inner index bounds of this lane inside [lo, hi).
-  const uint64_t ilo64 = a.lo > base ? a.lo - base : 0;
-  const uint64_t ihi64 = a.hi - base;  // > 0 because o < ceil(hi / 3^J)
-  const uint32_t ilo = uint32_t(ilo64 < a.inner_count ? ilo64 : a.inner_count);
-  const uint32_t ihi = uint32_t(ihi64 < a.inner_count ? ihi64 : a.inner_count);
+  uint64_t xo64;  // index weight of the outer digits
+  decode_positions<N>(tab, o, J, N, ogn, ogq, xo64);
+  uint32_t ilo = 0, ihi = a.inner_count;
+  uint64_t base = 0;
+  if constexpr (!FULL) {
+    base = o * a.inner_count;
+    const uint64_t ilo64 = a.lo > base ? a.lo - base : 0;
+    const uint64_t ihi64 = a.hi - base;  // > 0 because o < ceil(hi / 3^J)
+    ilo = uint32_t(ilo64 < a.inner_count ? ilo64 : a.inner_count);
+    ihi = uint32_t(ihi64 < a.inner_count ? ihi64 : a.inner_count);
+  }
+  const I xo = I(xo64);
+  I bx = I(best_x);
   M ign = 0, igq = 0;  // inner modes: the same in every lane of the wave
+  I xi = 0;            // index weight of the inner digits
   for (uint32_t i = 0; i < a.inner_count; ++i) {
-    if (i >= ilo && i < ihi) {
+    if (FULL || (i >= ilo && i < ihi)) {
       const uint32_t ms = evaluate<N>(tab, lds, levels, budget, ogn | ign, ogq | igq);
-      if (ms < best_ms) {
-        best_ms = ms;
-        best_x = base + i;
+      if constexpr (FULL) {
+        if (ms <= best_ms) {
+          const I x = xo + xi;
+          if (ms < best_ms || x < bx) {
+            best_ms = ms;
+            bx = x;
+          }
+        }
+      } else {
+        if (ms < best_ms) {
+          best_ms = ms;
+          best_x = base + i;
+        }
       }
     }
-    // odometer step on the inner digits (original tools 0..J-1)
+    // odometer step on the inner digits
     for (uint32_t j = 0; j < J; ++j) {
-      const M b = M(1) << tab[kPosBase + j];
-      if (igq & b) {
+      const M b = M(1) << tab[kEnumLabBase + j];
+      const I w = I(uint64_t(tab[kEnumWeightBase + 2 * j]) |
+                    (uint64_t(tab[kEnumWeightBase + 2 * j + 1]) << 32));
+      if (igq & b) {  // 2 -> 0, carry
         igq &= ~b;
+        xi -= 2 * w;
         continue;
       }
+      xi += w;
       if (ign & b) {
         ign &= ~b;
         igq |= b;
@@ -376,14 +482,17 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
       break;
     }
   }
+  if constexpr (FULL) {
+    if (best_ms != kInf) best_x = bx;
+  }
 }
 
 // Exhaustive search.  Block b serves table b / blocks_per_table and walks its
 // work items (kBlock consecutive outer combinations each) with a stride of
 // blocks_per_table.  Each lane keeps its own (makespan, index) minimum; the
 // block's minimum goes to partials[b].
-template <int N>
-__global__ __launch_bounds__(kBlock) void search_kernel(SearchArgs a) {
+template <int N, bool FULL>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(DEVMAP_SEARCH_WAVES))) void search_kernel(SearchArgs a) {
   __shared__ uint32_t s_lds[lds_words<N>()];
   const uint32_t table = blockIdx.x / a.blocks_per_table;
   const uint32_t bb = blockIdx.x - table * a.blocks_per_table;
@@ -393,7 +502,7 @@ __global__ __launch_bounds__(kBlock) void search_kernel(SearchArgs a) {
   uint32_t best_ms = kInf;
   uint64_t best_x = ~0ull;
   for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-    lane_search<N>(a, tab, s_lds, item, threadIdx.x, best_ms, best_x);
+    lane_search<N, FULL>(a, tab, s_lds, item, threadIdx.x, best_ms, best_x);
 
   block_min(best_ms, best_x);
   if (threadIdx.x == 0) {
@@ -435,7 +544,10 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
 template <int N>
 hipError_t launch_search_n(const SearchArgs& a, hipStream_t s) {
   const uint32_t blocks = a.n_tables * a.blocks_per_table;
-  hipLaunchKernelGGL(search_kernel<N>, dim3(blocks), dim3(kBlock), 0, s, a);
+  if (a.full_range)
+    hipLaunchKernelGGL((search_kernel<N, true>), dim3(blocks), dim3(kBlock), 0, s, a);
+  else
+    hipLaunchKernelGGL((search_kernel<N, false>), dim3(blocks), dim3(kBlock), 0, s, a);
   return hipGetLastError();
 }
 
