@@ -45,7 +45,7 @@ extern "C" {
 #define SCHED_E_EDGE (-4)      /* edge endpoint out of range, or a self-loop */
 #define SCHED_E_CYCLE (-5)     /* the edges contain a cycle */
 #define SCHED_E_RANGE (-6)     /* lo >= hi or hi > 3^N; replica map out of range */
-#define SCHED_E_OVERFLOW (-7)  /* the worst-case makespan bound reaches 2^31 us,
+#define SCHED_E_OVERFLOW (-7)  /* the worst-case makespan bound reaches 2^30 us,
                                   or (N+1)*(budget+1) reaches 2^32: the device
                                   path keeps times and VRAM sums in 32 bits */
 #define SCHED_E_WORKSPACE (-8) /* workspace null, misaligned (256 B) or too small */

@@ -95,7 +95,7 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
       }
     }
     bound += (unsigned __int128)longest + (unsigned __int128)uint64_t(xfer);
-    if (bound >= ((unsigned __int128)1 << 31)) return SCHED_E_OVERFLOW;
+    if (bound >= ((unsigned __int128)1 << 30)) return SCHED_E_OVERFLOW;
 
     uint32_t* rec = out + kHdrWords + kToolWords * uint32_t(i);
     rec[kToolCpu] = uint32_t(cpu);

@@ -100,15 +100,17 @@ constexpr uint32_t lds_words() { return lds_pos_off<N>() + uint32_t(N); }
 // one event time per call of step().
 //
 // gnm / gqm: tools on gpu_now / gpu_queue (internal labels; the rest run on
-// the CPU).  Per-tool state lives in two register arrays; times stay below
-// 2^31 - 1 (a creation-time guard), which frees the top bit as a tag:
-//   R[i]  ready time of a waiting tool: r for gpu_now, r | 2^31 for
-//         gpu_queue; kNoReady (2^31 - 1) when not waiting
-//   F[i]  finish time of a started tool: f for a GPU tool, f | 2^31 for a
-//         CPU tool; 0 before it starts
-// Unsigned differences then answer every question with one compare: a GPU
-// tool runs at t iff F - (t+1) < 2^31 - (t+1); a queued tool is ready iff
-// R - 2^31 <= t; and so on.
+// the CPU).  A tool is first unresolved, then waiting (its ready time is
+// known), then started (its finish time is known); it never needs both times
+// at once, so one register T[i] per tool holds its state.  Times stay below
+// H = 2^30 (a creation-time guard), which leaves the two top bits as a tag:
+//   0            unresolved
+//   f            started on the GPU, finishing at f (f >= 1)
+//   H + r        waiting gpu_now tool, ready at r
+//   2H + r       waiting gpu_queue tool, ready at r
+//   3H + f       CPU tool finishing at f
+// One unsigned difference then answers each question: a GPU tool runs at t
+// iff T - (t+1) < H - (t+1); a queued tool is ready iff T - 2H <= t; and so on.
 // A CPU tool starts the moment its inputs arrive and neither slows nor blocks
 // anything, so it is resolved as soon as all its predecessors have started;
 // the ascending sweep over topological labels resolves chains of CPU tools
@@ -118,7 +120,7 @@ constexpr uint32_t lds_words() { return lds_pos_off<N>() + uint32_t(N); }
 //      concurrency k and the VRAM in use (over the budget: out of memory);
 //      if no queued tool is running, the ready queued tool with the smallest
 //      (ready time, original number) is admitted when it fits;
-//   B. in label order: starters get F = t + dur[k], fixed for their life;
+//   B. in label order: starters get f = t + dur[k], fixed for their life;
 //      tools whose predecessors have all started get their ready time
 //      r = max over u -> i of finish(u) (+ xfer_i across devices); and the
 //      next event is accumulated: gpu_now and gpu_queue ready times after t,
@@ -126,46 +128,44 @@ constexpr uint32_t lds_words() { return lds_pos_off<N>() + uint32_t(N); }
 //      queue's own finish when the queue is busy).
 // A mapping needs at most 2N+1 passes: every pass after the first moves t to
 // a ready or finish time, and each tool has one of each.
-constexpr uint32_t kTag = 0x80000000u;
-constexpr uint32_t kNoReady = 0x7FFFFFFFu;
+constexpr uint32_t kH = 0x40000000u;  // 2^30: time limit and tag unit
+constexpr uint32_t kTagNow = kH;
+constexpr uint32_t kTagQueue = 2u * kH;
+constexpr uint32_t kTagCpu = 3u * kH;
 
 template <int N>
 struct Sim {
   using M = MaskT<N>;
-  uint32_t R[N], F[N];
+  uint32_t T[N];
   M gnm, gqm;
-  M started;   // started GPU tools and resolved CPU tools
-  M resolved;  // tools whose ready time is known
+  M started;      // started GPU tools and resolved CPU tools
   uint32_t t;
   uint32_t qfin;  // finish of the running queued tool (0: none)
-  uint32_t minq;  // earliest ready time of a waiting queued tool (>= 2^31: none)
-  int pass;       // passes done; -1: statically infeasible
+  uint32_t minq;  // earliest ready time of a waiting queued tool (>= H: none)
+  bool dead;      // statically infeasible
 
   __host__ __device__ __forceinline__ void init(const uint32_t* __restrict__ tab, M gn, M gq) {
     gnm = gn;
     gqm = gq;
 #pragma unroll
-    for (int i = 0; i < N; ++i) {
-      R[i] = kNoReady;
-      F[i] = 0;
-    }
+    for (int i = 0; i < N; ++i) T[i] = 0;
     started = 0;
-    resolved = 0;
     t = 0;
     qfin = 0;
     minq = kInf;
     // a GPU mode whose footprint exceeds the budget never fits
-    pass = ((gn | gq) & load_mask<N>(Tab{tab}, kHdrBigLo)) ? -1 : 0;
+    dead = ((gn | gq) & load_mask<N>(Tab{tab}, kHdrBigLo)) != 0;
   }
 
-  // One pass.  Returns true when the mapping is settled; ms then holds its
-  // makespan, or kInf if it is infeasible.
+  // Pass number `pass` (wave-uniform: the lanes of a wave start their
+  // mappings together).  Returns true when the mapping is settled; ms then
+  // holds its makespan, or kInf if it is infeasible.
   __host__ __device__ __forceinline__ bool step(const uint32_t* __restrict__ tab,
                                                 const uint32_t* __restrict__ lds,
-                                                uint32_t levels, uint32_t budget,
+                                                uint32_t levels, uint32_t budget, int pass,
                                                 uint32_t& ms) {
     ms = kInf;
-    if (pass < 0 || pass > 2 * N + 1) return true;
+    if (dead) return true;
     const M ALL = all_tools<N>();
     const M gpum = gnm | gqm;
     const uint32_t* s_dur = lds;
@@ -173,13 +173,14 @@ struct Sim {
     const uint32_t* s_pos = lds + lds_pos_off<N>();
     const Tab tp = fresh(tab);
     const uint32_t t1 = t + 1u;
-    const uint32_t lim = kTag - t1;  // F - t1 < lim: a GPU tool running at t
+    const uint32_t lim = kH - t1;  // d = x - t1 < lim: x is a time after t
+    const uint32_t now_t = kTagNow + t;
 
     // A. concurrency and VRAM at t, after releases and immediate starts
     uint32_t in_use = 0, k = 0;
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const bool on = (F[i] - t1 < lim) | (R[i] == t);
+      const bool on = (T[i] - t1 < lim) | (T[i] == now_t);
       in_use += on ? tp[kHdrWords + kToolWords * i + kToolMem] : 0u;
       k += on ? 1u : 0u;
     }
@@ -191,7 +192,7 @@ struct Sim {
         uint32_t hR = kInf;
 #pragma unroll
         for (int i = 0; i < N; ++i) {
-          const uint32_t rq = R[i] - kTag;  // queued: its ready time; others wrap high
+          const uint32_t rq = T[i] - kTagQueue;  // a queued tool's ready time; others wrap high
           const bool rd = rq <= t;
           waiting += rd ? 1u : 0u;
           hR = umin32(hR, rd ? rq : kInf);
@@ -199,7 +200,8 @@ struct Sim {
         uint32_t hO = kInf;  // FIFO ties go to the lowest original number
 #pragma unroll
         for (int i = 0; i < N; ++i)
-          hO = umin32(hO, R[i] - kTag == hR ? tp[kHdrWords + kToolWords * i + kToolOrig] : kInf);
+          hO = umin32(hO, T[i] - kTagQueue == hR ? tp[kHdrWords + kToolWords * i + kToolOrig]
+                                                  : kInf);
         const uint32_t lab = s_pos[hO];
         if (s_mem[lab] <= budget - in_use) {
           hsel = lab;
@@ -220,13 +222,11 @@ struct Sim {
       const M bi = M(1) << i;
       const bool adm = (hsel == uint32_t(i));
       const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
-      if (R[i] == t || adm) {
-        const uint32_t d = s_dur[(uint32_t(i) * 2u + (adm ? 1u : 0u)) * levels + lev];
-        F[i] = t + d;
-        R[i] = kNoReady;
+      if (T[i] == now_t || adm) {
+        T[i] = t + s_dur[(uint32_t(i) * 2u + (adm ? 1u : 0u)) * levels + lev];
         started |= bi;
-        if (adm) qfin = F[i];
-      } else if (((started & pm) | (resolved & bi)) == pm) {
+        if (adm) qfin = T[i];
+      } else if (T[i] == 0 && (started & pm) == pm) {
         const Tab rec = fresh(tab) + (kHdrWords + kToolWords * i);
         uint32_t g = 0, c = 0;  // latest GPU finish; latest finish overall
         // Predecessors carry smaller labels; the mask test is wave-uniform.
@@ -234,51 +234,49 @@ struct Sim {
         for (int u = 0; u < i; ++u) {
           if ((pm >> u) & 1) {  // scalar branch: no vector work for non-edges
             DEVMAP_KEEP_BRANCH();
-            const uint32_t f = F[u];
-            g = umax32(g, f < kTag ? f : 0u);
-            c = umax32(c, f);  // CPU finishes carry the tag, so they dominate
+            const uint32_t f = T[u];
+            g = umax32(g, f < kH ? f : 0u);
+            c = umax32(c, f);  // CPU finishes carry the top tag, so they dominate
           }
         }
-        c = c >= kTag ? c - kTag : 0u;  // latest CPU finish (0: none)
+        c = c >= kTagCpu ? c - kTagCpu : 0u;  // latest CPU finish (0: none)
         const uint32_t xw = rec[kToolXfer];
         const bool on_gpu = (gpum & bi) != 0;
         const uint32_t r = on_gpu ? umax32(g, c ? c + xw : 0u) : umax32(c, g ? g + xw : 0u);
-        resolved |= bi;
         if (!on_gpu) {
-          F[i] = (r + rec[kToolCpu]) | kTag;
+          T[i] = kTagCpu + r + rec[kToolCpu];
           started |= bi;
-        } else if (gnm & bi) {
-          R[i] = r;
         } else {
-          R[i] = r | kTag;
+          T[i] = ((gnm & bi) ? kTagNow : kTagQueue) + r;
         }
       }
-      tn = umin32(tn, R[i]);             // gpu_now ready times (queued ones are tagged high)
-      const uint32_t rq = R[i] - kTag;  // queued ready time; others wrap high
-      minq = umin32(minq, rq);
-      tq = umin32(tq, rq - t1);          // wraps for ready times <= t
-      tf = umin32(tf, F[i] - t1);        // below lim only for GPU tools running after t
+      const uint32_t x = T[i];
+      tn = umin32(tn, x - kTagNow - t1);     // gpu_now ready after t
+      const uint32_t rq = x - kTagQueue;
+      minq = umin32(minq, rq);               // queued ready time (>= H: none)
+      tq = umin32(tq, rq - t1);              // queued ready after t
+      tf = umin32(tf, x - t1);               // GPU finish after t
     }
-    ++pass;
     if (started == ALL) {
       uint32_t m = 0;
 #pragma unroll
-      for (int i = 0; i < N; ++i) m = umax32(m, F[i] & ~kTag);
+      for (int i = 0; i < N; ++i) m = umax32(m, T[i] & (kH - 1u));
       ms = m;
       return true;
     }
-    if (pass == 1) return false;  // sources resolved: now the events at t = 0
-    if (tn >= kNoReady) tn = kInf;
-    if (tq < kTag) tn = umin32(tn, tq + t1);
+    if (pass == 0) return false;  // sources resolved: now the events at t = 0
+    uint32_t next = kInf;
+    if (tn < lim) next = tn + t1;
+    if (tq < lim) next = umin32(next, tq + t1);
     if (waiting != 0) {
       if (qfin > t) {
-        tn = umin32(tn, qfin);     // queue busy: wait for it
+        next = umin32(next, qfin);     // queue busy: wait for it
       } else if (tf < lim) {
-        tn = umin32(tn, tf + t1);  // blocked on VRAM: wait for a release
+        next = umin32(next, tf + t1);  // blocked on VRAM: wait for a release
       }
     }
-    if (tn == kInf) return true;  // a queued tool can never fit: infeasible
-    t = tn;
+    if (next == kInf) return true;  // a queued tool can never fit: infeasible
+    t = next;
     return false;
   }
 };
@@ -292,8 +290,8 @@ __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict
   Sim<N> sim;
   sim.init(tab, gnm, gqm);
   uint32_t ms = kInf;
-  while (!sim.step(tab, lds, levels, budget, ms)) {
-  }
+  for (int pass = 0; pass < 2 * N + 2; ++pass)
+    if (sim.step(tab, lds, levels, budget, pass, ms)) break;
   return ms;
 }
 
@@ -398,7 +396,7 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
 
 // Waves per SIMD the search kernel is compiled for (the register budget).
 #ifndef DEVMAP_SEARCH_WAVES
-#define DEVMAP_SEARCH_WAVES 6
+#define DEVMAP_SEARCH_WAVES 7
 #endif
 
 // Index arithmetic: 3^20 < 2^32, so up to 20 tools an index fits 32 bits.
