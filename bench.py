@@ -6,6 +6,10 @@ schedule evaluation and (makespan, index) argmin, all in the HIP library.
 Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps 5] [--warmup 1] [--no-cpu-baseline]
+                    [--config 0..4]
+
+--config selects another synthetic workload for the same measurement: 0-2 a
+single search, 4 one batched call (13 scenarios x 64 replicas x 3^14).
 """
 from __future__ import annotations
 
@@ -23,6 +27,23 @@ sys.path.insert(0, ROOT)
 CUS, LANES_PER_CU, CLOCK_HZ = 256, 64, 2.4e9
 VALU_PEAK_OPS = CUS * LANES_PER_CU * CLOCK_HZ  # 3.93e13 int32 lane-ops/s
 HEADLINE_CONFIG = 3
+
+# HBM bytes per launch of search_kernel<19, full range> on the headline search:
+# rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
+# reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
+# whose SHA-256 is recorded; after any change the figure is reported as null.
+TRAFFIC_BYTES = 1657096466
+TRAFFIC_KERNEL_SHA256 = "47d2ae6fa7363cb628a1b5504646ab18105e50b7ec2f107941b449dd48b0501b"
+KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
+
+
+def kernel_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def algorithmic_ops_per_mapping(n_tools: int, n_edges: int) -> float:
@@ -53,7 +74,7 @@ def cpu_baseline(inst, target_seconds: float = 12.0):
     Q.argmin(0, count, threads=threads)
     dt = time.perf_counter() - t0
     return {"value": count / dt, "unit": "mappings/s", "cores": threads, "kind": "oracle",
-            "sample": f"mapping indices [0, {count}) of the same 3^19 search "
+            "sample": f"mapping indices [0, {count}) of the same search "
                       f"({dt:.1f} s on {threads} host threads)"}
 
 
@@ -63,6 +84,7 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--config", type=int, default=HEADLINE_CONFIG, choices=range(5))
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only run one plain device-to-device copy of this many MiB "
                          "(the reference kernel for scaling HBM byte counters)")
@@ -87,15 +109,29 @@ def main():
     import paper_2607_22242_amd as S
     from workloads import synth
 
-    inst = synth.load(HEADLINE_CONFIG)
-    P = S.Problem.from_instance(inst)
-    ws = S.workspace([P.handle])
+    inst = synth.load(args.config)
     stream = torch.cuda.current_stream()
-    total = P.n_mappings
+    if args.config == 4:
+        scen = inst["scenarios"]
+        problems = [S.Problem.from_instance(sc) for sc in scen]
+        handles = [p.handle for p in problems]
+        rp = [si for si, sc in enumerate(scen) for _ in sc["replicas"]]
+        lat = [rep for sc in scen for rep in sc["replicas"]]
+        ws = S.workspace(handles, len(rp))
+        total = len(rp) * problems[0].n_mappings
+        n_tools = problems[0].n
+        n_edges = sum(len(sc["edges"]) for sc in scen) / len(scen)
+        run = lambda: S.sched_eval_batch(handles, rp, lat, ws, stream)  # noqa: E731
+    else:
+        P = S.Problem.from_instance(inst)
+        ws = S.workspace([P.handle])
+        total = P.n_mappings
+        n_tools, n_edges = P.n, len(inst["edges"])
+        run = lambda: S.sched_bruteforce_argmin(P.handle, 0, total, ws, stream)  # noqa: E731
 
     result = None
     for _ in range(args.warmup):
-        result = S.sched_bruteforce_argmin(P.handle, 0, total, ws, stream)
+        result = run()
     torch.cuda.synchronize()
 
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -103,7 +139,7 @@ def main():
     t0 = time.perf_counter()
     for i in range(args.steps):
         starts[i].record(stream)
-        result = S.sched_bruteforce_argmin(P.handle, 0, total, ws, stream)
+        result = run()
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -111,18 +147,34 @@ def main():
     avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
 
     value = total * args.steps / wall
-    ops = algorithmic_ops_per_mapping(inst["n_tools"], len(inst["edges"]))
+    ops = algorithmic_ops_per_mapping(n_tools, n_edges)
     achieved = ops * total / avg_launch_s
 
-    check = {"best_index": result[0], "makespan_us": result[1]}
     exp_path = os.path.join(ROOT, "tests", "golden", "expected_configs.json")
+    expected = None
     if os.path.exists(exp_path):
         with open(exp_path) as f:
-            e = json.load(f).get(f"config{HEADLINE_CONFIG}")
-        if e:
-            check["matches_oracle"] = (result[0] == e["best_index"] and
-                                       result[1] == e["makespan_us"])
+            expected = json.load(f).get(f"config{args.config}")
+    if args.config == 4:
+        check = {"replicas": len(result)}
+        if expected:
+            want = [tuple(x) for row in expected["results"] for x in row]
+            check["matches_oracle"] = [tuple(r) for r in result] == want
+    else:
+        check = {"best_index": result[0], "makespan_us": result[1]}
+        if expected:
+            check["matches_oracle"] = (result[0] == expected["best_index"] and
+                                       result[1] == expected["makespan_us"])
 
+    workloads = {
+        0: "chain8: 8-tool serial chain, 3^8 mappings",
+        1: "layered12: 12 tools in 3 layers of 4, 3^12 mappings",
+        2: "memlayered16: 16 tools in 4 layers of 4, budget a quarter of the footprints, "
+           "3^16 mappings",
+        3: "mixed19: 19-tool random DAG (15 edges), 3^19 mappings, VRAM budget 49152 MiB, "
+           "4-level Q16 contention",
+        4: "batch13x64: 13 scenarios x 64 perturbed replicas, 14 tools, 3^14 mappings each",
+    }
     line = {
         "metric": "mappings evaluated/sec (3^N brute force, N=19) + % of VALU peak",
         "value": value,
@@ -136,17 +188,17 @@ def main():
         "vs_baseline": None,
         "dtype": "u32",
         "data": "synthetic",
-        "config": {"workload": "mixed19: 19-tool random DAG (15 edges), 3^19 mappings, "
-                               "VRAM budget 49152 MiB, 4-level Q16 contention",
-                   "n_tools": inst["n_tools"], "mappings_per_step": total,
-                   "parallelism": "single GPU"},
+        "config": {"workload": workloads[args.config], "n_tools": n_tools,
+                   "mappings_per_step": total, "parallelism": "single GPU"},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12,
                      "peak": VALU_PEAK_OPS / 1e12, "unit": "Tops/s (int32 VALU lane-ops)",
-                     "frac": achieved / VALU_PEAK_OPS, "traffic": None,
+                     "frac": achieved / VALU_PEAK_OPS,
+                     "traffic": (TRAFFIC_BYTES if args.config == HEADLINE_CONFIG and
+                                 kernel_sha256() == TRAFFIC_KERNEL_SHA256 else None),
                      "ops_per_mapping": ops, "kernel_ms": avg_launch_s * 1e3},
         "check": check,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.config != 4:
         line["cpu_baseline"] = cpu_baseline(inst)
     print(json.dumps(line), flush=True)
 
