@@ -56,6 +56,17 @@ __host__ __device__ __forceinline__ Tab fresh(const uint32_t* p) {
   return Tab{p};
 }
 
+// A wave-uniform value the optimiser must not carry across this point: its
+// bit tests are recomputed in scalar registers where they are used rather
+// than kept live as lane masks (which would crowd the scalar register file).
+template <class M>
+__host__ __device__ __forceinline__ M opaque(M x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("" : "+s"(x));
+#endif
+  return x;
+}
+
 // An empty side effect: keeps a wave-uniform branch a branch instead of
 // letting the optimiser turn its body into per-lane selects.
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -96,6 +107,31 @@ constexpr uint32_t lds_pos_off() { return lds_mem_off<N>() + uint32_t(N); }
 template <int N>
 constexpr uint32_t lds_words() { return lds_pos_off<N>() + uint32_t(N); }
 
+// Bitwise OR of x over the active lanes of the calling wave, through one LDS
+// word per wave (slot).  Lanes that have left the calling loop simply do not
+// contribute, so the result is right under divergence too.  A host build has
+// one lane per "wave": the result is x itself.
+template <class M>
+__host__ __device__ __forceinline__ M wave_or(M x, M* slot) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __hip_atomic_store(slot, M(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+  __builtin_amdgcn_wave_barrier();
+  __hip_atomic_fetch_or(slot, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+  __builtin_amdgcn_wave_barrier();
+  const M r = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+  __builtin_amdgcn_wave_barrier();
+  if constexpr (sizeof(M) == 4) {
+    return __builtin_amdgcn_readfirstlane(r);
+  } else {
+    return (uint64_t(__builtin_amdgcn_readfirstlane(uint32_t(r >> 32))) << 32) |
+           __builtin_amdgcn_readfirstlane(uint32_t(r));
+  }
+#else
+  (void)slot;
+  return x;
+#endif
+}
+
 // Event-driven schedule of one mapping (the schedule model in full), advanced
 // one event time per call of step().
 //
@@ -126,6 +162,11 @@ constexpr uint32_t lds_words() { return lds_pos_off<N>() + uint32_t(N); }
 //      next event is accumulated: gpu_now and gpu_queue ready times after t,
 //      plus GPU finishes when a ready queued tool is still waiting (only the
 //      queue's own finish when the queue is busy).
+// Work is skipped for tools that are settled in every lane of the wave: a
+// pass only visits tools that some lane still has waiting or running (the
+// wave-wide OR of the lanes' active masks) and, for resolution, tools that
+// some lane has not resolved yet.  A settled tool contributes nothing to a
+// pass, so skipping it changes no result.
 // A mapping needs at most 2N+1 passes: every pass after the first moves t to
 // a ready or finish time, and each tool has one of each.
 constexpr uint32_t kH = 0x40000000u;  // 2^30: time limit and tag unit
@@ -138,7 +179,9 @@ struct Sim {
   using M = MaskT<N>;
   uint32_t T[N];
   M gnm, gqm;
-  M started;      // started GPU tools and resolved CPU tools
+  M started;   // started GPU tools and resolved CPU tools
+  M resolved;  // tools whose ready time is known
+  M done;      // CPU tools and GPU tools seen finished
   uint32_t t;
   uint32_t qfin;  // finish of the running queued tool (0: none)
   uint32_t minq;  // earliest ready time of a waiting queued tool (>= H: none)
@@ -150,6 +193,8 @@ struct Sim {
 #pragma unroll
     for (int i = 0; i < N; ++i) T[i] = 0;
     started = 0;
+    resolved = 0;
+    done = 0;
     t = 0;
     qfin = 0;
     minq = kInf;
@@ -159,11 +204,12 @@ struct Sim {
 
   // Pass number `pass` (wave-uniform: the lanes of a wave start their
   // mappings together).  Returns true when the mapping is settled; ms then
-  // holds its makespan, or kInf if it is infeasible.
+  // holds its makespan, or kInf if it is infeasible.  slot: this wave's LDS
+  // word for the wave-wide masks.
   __host__ __device__ __forceinline__ bool step(const uint32_t* __restrict__ tab,
                                                 const uint32_t* __restrict__ lds,
                                                 uint32_t levels, uint32_t budget, int pass,
-                                                uint32_t& ms) {
+                                                M* slot, uint32_t& ms) {
     ms = kInf;
     if (dead) return true;
     const M ALL = all_tools<N>();
@@ -175,14 +221,21 @@ struct Sim {
     const uint32_t t1 = t + 1u;
     const uint32_t lim = kH - t1;  // d = x - t1 < lim: x is a time after t
     const uint32_t now_t = kTagNow + t;
+    // tools some lane of the wave has waiting or running / not resolved
+    const M wa = wave_or<M>(resolved & ~done, slot);
+    const M wu = wave_or<M>(ALL & ~resolved, slot);
 
     // A. concurrency and VRAM at t, after releases and immediate starts
     uint32_t in_use = 0, k = 0;
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const bool on = (T[i] - t1 < lim) | (T[i] == now_t);
-      in_use += on ? tp[kHdrWords + kToolWords * i + kToolMem] : 0u;
-      k += on ? 1u : 0u;
+      if ((wa >> i) & 1) {
+        const uint32_t x = T[i];
+        const bool on = (x - t1 < lim) | (x == now_t);
+        in_use += on ? tp[kHdrWords + kToolWords * i + kToolMem] : 0u;
+        k += on ? 1u : 0u;
+        if (x - 1u < t) done |= M(1) << i;  // a GPU tool finished by t
+      }
     }
     if (in_use > budget) return true;  // out of memory: infeasible
     uint32_t hsel = kInf;              // label of the queued tool admitted at t
@@ -190,18 +243,23 @@ struct Sim {
     if (minq <= t) {
       if (qfin <= t) {
         uint32_t hR = kInf;
+        const M wa_q = opaque(wa);
 #pragma unroll
         for (int i = 0; i < N; ++i) {
-          const uint32_t rq = T[i] - kTagQueue;  // a queued tool's ready time; others wrap high
-          const bool rd = rq <= t;
-          waiting += rd ? 1u : 0u;
-          hR = umin32(hR, rd ? rq : kInf);
+          if ((wa_q >> i) & 1) {
+            const uint32_t rq = T[i] - kTagQueue;  // a queued tool's ready time; others wrap high
+            const bool rd = rq <= t;
+            waiting += rd ? 1u : 0u;
+            hR = umin32(hR, rd ? rq : kInf);
+          }
         }
         uint32_t hO = kInf;  // FIFO ties go to the lowest original number
+        const M wa_t = opaque(wa);
 #pragma unroll
         for (int i = 0; i < N; ++i)
-          hO = umin32(hO, T[i] - kTagQueue == hR ? tp[kHdrWords + kToolWords * i + kToolOrig]
-                                                  : kInf);
+          if ((wa_t >> i) & 1)
+            hO = umin32(hO, T[i] - kTagQueue == hR ? tp[kHdrWords + kToolWords * i + kToolOrig]
+                                                    : kInf);
         const uint32_t lab = s_pos[hO];
         if (s_mem[lab] <= budget - in_use) {
           hsel = lab;
@@ -217,45 +275,55 @@ struct Sim {
     // B. starts, resolution, next event
     uint32_t tn = kInf, tq = kInf, tf = kInf;
     minq = kInf;
+    const M wa_b = opaque(wa), wu_b = opaque(wu);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       const M bi = M(1) << i;
-      const bool adm = (hsel == uint32_t(i));
-      const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
-      if (T[i] == now_t || adm) {
-        T[i] = t + s_dur[(uint32_t(i) * 2u + (adm ? 1u : 0u)) * levels + lev];
-        started |= bi;
-        if (adm) qfin = T[i];
-      } else if (T[i] == 0 && (started & pm) == pm) {
-        const Tab rec = fresh(tab) + (kHdrWords + kToolWords * i);
-        uint32_t g = 0, c = 0;  // latest GPU finish; latest finish overall
-        // Predecessors carry smaller labels; the mask test is wave-uniform.
-#pragma unroll
-        for (int u = 0; u < i; ++u) {
-          if ((pm >> u) & 1) {  // scalar branch: no vector work for non-edges
-            DEVMAP_KEEP_BRANCH();
-            const uint32_t f = T[u];
-            g = umax32(g, f < kH ? f : 0u);
-            c = umax32(c, f);  // CPU finishes carry the top tag, so they dominate
-          }
-        }
-        c = c >= kTagCpu ? c - kTagCpu : 0u;  // latest CPU finish (0: none)
-        const uint32_t xw = rec[kToolXfer];
-        const bool on_gpu = (gpum & bi) != 0;
-        const uint32_t r = on_gpu ? umax32(g, c ? c + xw : 0u) : umax32(c, g ? g + xw : 0u);
-        if (!on_gpu) {
-          T[i] = kTagCpu + r + rec[kToolCpu];
+      if ((wa_b >> i) & 1) {
+        const bool adm = (hsel == uint32_t(i));
+        if (T[i] == now_t || adm) {
+          T[i] = t + s_dur[(uint32_t(i) * 2u + (adm ? 1u : 0u)) * levels + lev];
           started |= bi;
-        } else {
-          T[i] = ((gnm & bi) ? kTagNow : kTagQueue) + r;
+          if (adm) qfin = T[i];
         }
       }
-      const uint32_t x = T[i];
-      tn = umin32(tn, x - kTagNow - t1);     // gpu_now ready after t
-      const uint32_t rq = x - kTagQueue;
-      minq = umin32(minq, rq);               // queued ready time (>= H: none)
-      tq = umin32(tq, rq - t1);              // queued ready after t
-      tf = umin32(tf, x - t1);               // GPU finish after t
+      if ((wu_b >> i) & 1) {
+        const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
+        if (T[i] == 0 && (started & pm) == pm) {
+          const Tab rec = fresh(tab) + (kHdrWords + kToolWords * i);
+          uint32_t g = 0, c = 0;  // latest GPU finish; latest finish overall
+          // Predecessors carry smaller labels; the mask test is wave-uniform.
+#pragma unroll
+          for (int u = 0; u < i; ++u) {
+            if ((pm >> u) & 1) {  // scalar branch: no vector work for non-edges
+              DEVMAP_KEEP_BRANCH();
+              const uint32_t f = T[u];
+              g = umax32(g, f < kH ? f : 0u);
+              c = umax32(c, f);  // CPU finishes carry the top tag, so they dominate
+            }
+          }
+          c = c >= kTagCpu ? c - kTagCpu : 0u;  // latest CPU finish (0: none)
+          const uint32_t xw = rec[kToolXfer];
+          const bool on_gpu = (gpum & bi) != 0;
+          const uint32_t r = on_gpu ? umax32(g, c ? c + xw : 0u) : umax32(c, g ? g + xw : 0u);
+          resolved |= bi;
+          if (!on_gpu) {
+            T[i] = kTagCpu + r + rec[kToolCpu];
+            started |= bi;
+            done |= bi;
+          } else {
+            T[i] = ((gnm & bi) ? kTagNow : kTagQueue) + r;
+          }
+        }
+      }
+      if (((wa_b | wu_b) >> i) & 1) {
+        const uint32_t x = T[i];
+        tn = umin32(tn, x - kTagNow - t1);     // gpu_now ready after t
+        const uint32_t rq = x - kTagQueue;
+        minq = umin32(minq, rq);               // queued ready time (>= H: none)
+        tq = umin32(tq, rq - t1);              // queued ready after t
+        tf = umin32(tf, x - t1);               // GPU finish after t
+      }
     }
     if (started == ALL) {
       uint32_t m = 0;
@@ -281,17 +349,19 @@ struct Sim {
   }
 };
 
-// Makespan of one mapping, or kInf if it is infeasible.
+// Makespan of one mapping, or kInf if it is infeasible.  slot: the calling
+// wave's LDS word (see wave_or).
 template <int N>
 __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict__ tab,
                                                       const uint32_t* __restrict__ lds,
                                                       uint32_t levels, uint32_t budget,
-                                                      MaskT<N> gnm, MaskT<N> gqm) {
+                                                      MaskT<N> gnm, MaskT<N> gqm,
+                                                      MaskT<N>* slot) {
   Sim<N> sim;
   sim.init(tab, gnm, gqm);
   uint32_t ms = kInf;
   for (int pass = 0; pass < 2 * N + 2; ++pass)
-    if (sim.step(tab, lds, levels, budget, pass, ms)) break;
+    if (sim.step(tab, lds, levels, budget, pass, slot, ms)) break;
   return ms;
 }
 
@@ -396,7 +466,7 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
 
 // Waves per SIMD the search kernel is compiled for (the register budget).
 #ifndef DEVMAP_SEARCH_WAVES
-#define DEVMAP_SEARCH_WAVES 7
+#define DEVMAP_SEARCH_WAVES 8
 #endif
 
 // Index arithmetic: 3^20 < 2^32, so up to 20 tools an index fits 32 bits.
@@ -417,7 +487,8 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
                                                      const uint32_t* __restrict__ tab,
                                                      const uint32_t* __restrict__ lds,
                                                      uint64_t item, uint32_t lane,
-                                                     uint32_t& best_ms, uint64_t& best_x) {
+                                                     MaskT<N>* slot, uint32_t& best_ms,
+                                                     uint64_t& best_x) {
   using M = MaskT<N>;
   using I = IdxT<N>;
   const uint64_t rel = item * kBlock + lane;
@@ -444,7 +515,7 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
   I xi = 0;            // index weight of the inner digits
   for (uint32_t i = 0; i < a.inner_count; ++i) {
     if (FULL || (i >= ilo && i < ihi)) {
-      const uint32_t ms = evaluate<N>(tab, lds, levels, budget, ogn | ign, ogq | igq);
+      const uint32_t ms = evaluate<N>(tab, lds, levels, budget, ogn | ign, ogq | igq, slot);
       if constexpr (FULL) {
         if (ms <= best_ms) {
           const I x = xo + xi;
@@ -492,6 +563,7 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 template <int N, bool FULL>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(DEVMAP_SEARCH_WAVES))) void search_kernel(SearchArgs a) {
   __shared__ uint32_t s_lds[lds_words<N>()];
+  __shared__ MaskT<N> s_wave[kBlock / 64];
   const uint32_t table = blockIdx.x / a.blocks_per_table;
   const uint32_t bb = blockIdx.x - table * a.blocks_per_table;
   const uint32_t* tab = a.tables + size_t(table) * a.table_stride;
@@ -500,7 +572,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(DEVMAP_S
   uint32_t best_ms = kInf;
   uint64_t best_x = ~0ull;
   for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-    lane_search<N, FULL>(a, tab, s_lds, item, threadIdx.x, best_ms, best_x);
+    lane_search<N, FULL>(a, tab, s_lds, item, threadIdx.x, &s_wave[threadIdx.x / 64], best_ms,
+                         best_x);
 
   block_min(best_ms, best_x);
   if (threadIdx.x == 0) {
@@ -520,6 +593,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
                                                       int64_t* __restrict__ out) {
   using M = MaskT<N>;
   __shared__ uint32_t s_lds[lds_words<N>()];
+  __shared__ MaskT<N> s_wave[kBlock / 64];
   stage_tables<N>(tab, s_lds);
   const uint32_t levels = tab[kHdrLevels];
   const uint32_t budget = tab[kHdrBudget];
@@ -530,7 +604,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
     if (x < n_mappings) {
       M gn, gq;
       decode_digits<N>(tab, x, 0, gn, gq);
-      const uint32_t ms = evaluate<N>(tab, s_lds, levels, budget, gn, gq);
+      const uint32_t ms = evaluate<N>(tab, s_lds, levels, budget, gn, gq, &s_wave[threadIdx.x / 64]);
       if (ms != kInf) r = int64_t(ms);
     }
     out[i] = r;
