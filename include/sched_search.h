@@ -133,6 +133,30 @@ int sched_eval_mappings(const sched_problem *p, const uint64_t *d_idx, int64_t n
                         int64_t *d_makespan, void *d_workspace, size_t ws_bytes,
                         void *hip_stream);
 
+/* One what-if probe around a base mapping. */
+typedef struct {
+    uint64_t index;      /* mapping probed */
+    int64_t makespan_us; /* INT64_MAX when infeasible */
+    int32_t kind;        /* 0: the base mapping, 1: single-tool move, 2: swap */
+    int32_t tool;        /* tool moved (-1 for the base) */
+    int32_t mode;        /* its new mode (0 cpu, 1 gpu_now, 2 gpu_queue) */
+    int32_t swap_tool;   /* swap: tool moved from gpu_now to gpu_queue; else -1 */
+} sched_probe;
+
+/* Bounded what-if exploration around base_index, the runtime monitor's active
+ * path (Section 3.2, Algorithm 1): the base mapping first; then for each tool
+ * i in order and each other mode a of tool i in the order cpu, gpu_now,
+ * gpu_queue, the single-tool move i -> a; right after a move to gpu_now that
+ * is infeasible (over the VRAM budget), one swap per tool j on gpu_now in the
+ * base mapping (ascending j): i -> gpu_now with j -> gpu_queue.
+ * lat: optional re-measured latencies (N entries, e.g. running averages) that
+ * replace the problem's own for these probes; null keeps the profiles.
+ * h_out: host array of capacity entries; capacity must be at least
+ * 1 + 2N + N(N-1).  *n_out receives the number of probes written. */
+int sched_eval_reprobes(const sched_problem *p, uint64_t base_index, const sched_lat *lat,
+                        void *d_workspace, size_t ws_bytes, void *hip_stream,
+                        sched_probe *h_out, int32_t capacity, int32_t *n_out);
+
 /* Static text for an error code. */
 const char *sched_strerror(int code);
 

@@ -144,3 +144,38 @@ def index_of(modes: Sequence[int]) -> int:
     for d in reversed(list(modes)):
         x = 3 * x + int(d)
     return x
+
+
+def reprobes(P: Problem, base_index: int) -> List[Dict]:
+    """Bounded what-if exploration around one mapping (Section 3.2,
+    Algorithm 1, the active path run when the mapping changed).
+
+    The base mapping is scored first.  Then, tool by tool, every other mode
+    of that tool is tried with the rest of the mapping held fixed; when the
+    move is to gpu_now and it does not fit the VRAM budget (the schedule is
+    infeasible), each tool that sits on gpu_now in the base mapping is tried
+    in its place on gpu_queue (a swap).  Every probe is scored by the same
+    schedule model as the search, on explicit per-tool modes.
+    """
+    d = modes_of(base_index, P.n)
+
+    def probe(kind, tool, mode, swap_tool, modes):
+        return {"index": index_of(modes), "makespan_us": P.schedule(modes)[0], "kind": kind,
+                "tool": tool, "mode": mode, "swap_tool": swap_tool}
+
+    out = [probe(0, -1, -1, -1, d)]
+    for i in range(P.n):
+        for a in (CPU, GPU_NOW, GPU_QUEUE):
+            if a == d[i]:
+                continue
+            moved = list(d)
+            moved[i] = a
+            r = probe(1, i, a, -1, moved)
+            out.append(r)
+            if r["makespan_us"] == INFEASIBLE and a == GPU_NOW:
+                for j in range(P.n):
+                    if d[j] == GPU_NOW:
+                        swapped = list(moved)
+                        swapped[j] = GPU_QUEUE
+                        out.append(probe(2, i, GPU_NOW, j, swapped))
+    return out

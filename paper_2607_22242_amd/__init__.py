@@ -5,6 +5,6 @@ include/sched_search.h); `binding` marshals arguments to it.
 """
 from .binding import (  # noqa: F401
     EXPORTED, INFEASIBLE, NO_INDEX, Problem, SchedError, sched_bruteforce_argmin,
-    sched_eval_batch, sched_eval_mappings, sched_num_mappings, sched_num_tools,
+    sched_eval_batch, sched_eval_mappings, sched_eval_reprobes, sched_num_mappings, sched_num_tools,
     sched_problem_create, sched_problem_destroy, sched_strerror, sched_workspace_bytes,
     workspace)

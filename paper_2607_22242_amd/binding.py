@@ -25,7 +25,8 @@ INFEASIBLE = (1 << 63) - 1
 
 EXPORTED = ["sched_problem_create", "sched_problem_destroy", "sched_num_tools",
             "sched_num_mappings", "sched_workspace_bytes", "sched_bruteforce_argmin",
-            "sched_eval_batch", "sched_eval_mappings", "sched_strerror"]
+            "sched_eval_batch", "sched_eval_mappings", "sched_eval_reprobes",
+            "sched_strerror"]
 
 
 class sched_tool(ctypes.Structure):
@@ -45,6 +46,12 @@ class sched_edge(ctypes.Structure):
 
 class sched_result(ctypes.Structure):
     _fields_ = [("best_index", ctypes.c_uint64), ("makespan_us", ctypes.c_int64)]
+
+
+class sched_probe(ctypes.Structure):
+    _fields_ = [("index", ctypes.c_uint64), ("makespan_us", ctypes.c_int64),
+                ("kind", ctypes.c_int32), ("tool", ctypes.c_int32),
+                ("mode", ctypes.c_int32), ("swap_tool", ctypes.c_int32)]
 
 
 class SchedError(RuntimeError):
@@ -87,6 +94,9 @@ def lib():
                                        ctypes.c_size_t, P, P]
         L.sched_eval_mappings.restype = ctypes.c_int
         L.sched_eval_mappings.argtypes = [P, P, ctypes.c_int64, P, P, ctypes.c_size_t, P]
+        L.sched_eval_reprobes.restype = ctypes.c_int
+        L.sched_eval_reprobes.argtypes = [P, ctypes.c_uint64, P, P, ctypes.c_size_t, P, P,
+                                          ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
         L.sched_strerror.restype = ctypes.c_char_p
         L.sched_strerror.argtypes = [ctypes.c_int]
         _lib = L
@@ -188,6 +198,25 @@ def sched_eval_mappings(handle, d_idx, d_makespan, workspace, stream=None) -> No
     wp, wb = _ws(workspace)
     _check(lib().sched_eval_mappings(handle, d_idx.data_ptr(), n, d_makespan.data_ptr(), wp, wb,
                                      _stream_ptr(stream)), "sched_eval_mappings")
+
+
+def sched_eval_reprobes(handle, base_index: int, workspace, lat=None,
+                        stream=None) -> List[dict]:
+    """What-if probes around base_index (see the header); each probe as a
+    dict with index, makespan_us, kind, tool, mode, swap_tool."""
+    n = sched_num_tools(handle)
+    cap = 1 + 2 * n + n * (n - 1)
+    out = (sched_probe * cap)()
+    got = ctypes.c_int32()
+    latp = None
+    if lat is not None:
+        latp = (sched_lat * n)(*[sched_lat(*map(int, r[:4])) for r in lat])
+    wp, wb = _ws(workspace)
+    _check(lib().sched_eval_reprobes(handle, base_index, latp, wp, wb, _stream_ptr(stream), out,
+                                     cap, ctypes.byref(got)), "sched_eval_reprobes")
+    return [{"index": out[k].index, "makespan_us": out[k].makespan_us, "kind": out[k].kind,
+             "tool": out[k].tool, "mode": out[k].mode, "swap_tool": out[k].swap_tool}
+            for k in range(got.value)]
 
 
 # ---------------------------------------------------------------------------

@@ -494,6 +494,99 @@ int sched_eval_mappings(const sched_problem* p, const uint64_t* d_idx, int64_t n
   return SCHED_OK;
 }
 
+int sched_eval_reprobes(const sched_problem* p, uint64_t base_index, const sched_lat* lat,
+                        void* d_workspace, size_t ws_bytes, void* hip_stream,
+                        sched_probe* h_out, int32_t capacity, int32_t* n_out) {
+  if (p == nullptr || h_out == nullptr || n_out == nullptr) return SCHED_E_NULL;
+  if (base_index >= p->n_mappings) return SCHED_E_RANGE;
+  const int n = p->n;
+  const int64_t worst = 1 + 2 * int64_t(n) + int64_t(n) * (n - 1);
+  if (capacity < worst) return SCHED_E_SIZE;
+  const Layout L = layout_for(size_t(p->table_words) * 4, partial_capacity(1), 1);
+  int rc = check_workspace(d_workspace, ws_bytes, L.total);
+  if (rc != SCHED_OK) return rc;
+
+  std::vector<uint32_t> table;
+  std::vector<uint64_t> idx;
+  std::vector<int64_t> ms;
+  try {
+    table.assign(p->table_words, 0u);
+    idx.reserve(size_t(worst));
+  } catch (const std::bad_alloc&) {
+    return SCHED_E_NOMEM;
+  }
+  if (lat != nullptr) {
+    rc = build_table(*p, lat, table.data());
+    if (rc != SCHED_OK) return rc;
+  } else {
+    table = p->table;
+  }
+  // Digits of the base mapping and the weight 3^v of each tool.
+  std::vector<int> d(n);
+  std::vector<uint64_t> w(n);
+  {
+    uint64_t x = base_index, pw = 1;
+    for (int v = 0; v < n; ++v) {
+      d[v] = int(x % 3u);
+      x /= 3u;
+      w[v] = pw;
+      pw *= 3u;
+    }
+  }
+  auto with = [&](uint64_t x, int v, int a) { return x - uint64_t(d[v]) * w[v] + uint64_t(a) * w[v]; };
+  // Every candidate, in the order of Algorithm 1 (swaps after their move).
+  struct Cand {
+    int kind, tool, mode, swap_tool;
+  };
+  std::vector<Cand> cands;
+  idx.push_back(base_index);
+  cands.push_back({0, -1, -1, -1});
+  for (int i = 0; i < n; ++i)
+    for (int a = 0; a < 3; ++a) {
+      if (a == d[i]) continue;
+      idx.push_back(with(base_index, i, a));
+      cands.push_back({1, i, a, -1});
+      if (a == 1)
+        for (int j = 0; j < n; ++j)
+          if (j != i && d[j] == 1) {
+            idx.push_back(with(with(base_index, i, 1), j, 2));
+            cands.push_back({2, i, 1, j});
+          }
+    }
+  const size_t m = idx.size();
+  ms.assign(m, 0);
+  // Scratch for the index list and the makespans: the partials region.
+  if (m * 16 > partial_capacity(1) * sizeof(Partial)) return SCHED_E_WORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  char* ws = static_cast<char*>(d_workspace);
+  uint64_t* d_idx = reinterpret_cast<uint64_t*>(ws + L.partials);
+  int64_t* d_ms = reinterpret_cast<int64_t*>(ws + L.partials + m * 8);
+  HIP_TRY(hipMemcpyAsync(ws + L.tables, table.data(), size_t(p->table_words) * 4,
+                         hipMemcpyHostToDevice, s));
+  HIP_TRY(hipMemcpyAsync(d_idx, idx.data(), m * 8, hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_eval(n, reinterpret_cast<const uint32_t*>(ws + L.tables), d_idx, int64_t(m),
+                      p->n_mappings, d_ms, s));
+  HIP_TRY(hipMemcpyAsync(ms.data(), d_ms, m * 8, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  // Keep a swap only when its move to gpu_now was infeasible.
+  int32_t out = 0;
+  int64_t move_ms = 0;
+  for (size_t k = 0; k < m; ++k) {
+    const Cand& c = cands[k];
+    if (c.kind == 1) move_ms = ms[k];
+    if (c.kind == 2 && move_ms != INT64_MAX) continue;
+    sched_probe& pr = h_out[out++];
+    pr.index = idx[k];
+    pr.makespan_us = ms[k];
+    pr.kind = c.kind;
+    pr.tool = c.tool;
+    pr.mode = c.mode;
+    pr.swap_tool = c.swap_tool;
+  }
+  *n_out = out;
+  return SCHED_OK;
+}
+
 const char* sched_strerror(int code) {
   switch (code) {
     case SCHED_OK: return "ok";

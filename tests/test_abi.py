@@ -100,6 +100,26 @@ def test_workspace_and_range_validation_before_any_device_work():
                                           fs)) == "SCHED_E_VALUE"
 
 
+def test_reprobe_validation_before_any_device_work():
+    P = S.Problem.from_instance(synth.load(0))
+    nbytes = S.sched_workspace_bytes([P.handle])
+    L = B.lib()
+    cap = 1 + 2 * 8 + 8 * 7
+    out = (B.sched_probe * cap)()
+    got = ctypes.c_int32(-7)
+    call = lambda base, ws, wb, c, lat=None, o=out: L.sched_eval_reprobes(  # noqa: E731
+        P.handle, base, lat, ws, wb, None, o, c, ctypes.byref(got))
+    name = lambda rc: B.ERRORS[rc]  # noqa: E731
+    assert name(call(3 ** 8, 256, nbytes, cap)) == "SCHED_E_RANGE"
+    assert name(call(0, 256, nbytes, cap - 1)) == "SCHED_E_SIZE"
+    assert name(call(0, 256, nbytes, cap, o=None)) == "SCHED_E_NULL"
+    assert name(call(0, 256, nbytes - 256, cap)) == "SCHED_E_WORKSPACE"
+    assert name(call(0, 128, nbytes, cap)) == "SCHED_E_WORKSPACE"
+    bad = (B.sched_lat * 8)(*[B.sched_lat(1, 1, 0, 0)] * 7 + [B.sched_lat(1, 0, 0, 0)])
+    assert name(call(0, 256, nbytes, cap, lat=bad)) == "SCHED_E_VALUE"
+    assert got.value == -7  # nothing written on error
+
+
 def test_strerror_covers_codes():
     for code, name in B.ERRORS.items():
         assert S.sched_strerror(code) != "unknown error", name

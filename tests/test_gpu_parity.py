@@ -259,3 +259,72 @@ def test_exact_workspace_and_repeat_calls(torch_cuda, O):
     a = S.sched_bruteforce_argmin(P.handle, 0, P.n_mappings, ws, s)
     b = S.sched_bruteforce_argmin(P.handle, 0, P.n_mappings, ws)
     assert a == b
+
+
+# ---------------------------------------------------------------------------
+# What-if re-scoring around one mapping (single-tool moves and swaps).
+
+
+def reprobe_bases(n, n_mappings, seed):
+    rng = np.random.default_rng(seed)
+    all_now = (3 ** n - 1) // 2  # every digit 1
+    bases = [0, n_mappings - 1, all_now]
+    bases += [int(x) for x in rng.integers(0, n_mappings, 6, dtype=np.uint64)]
+    return bases
+
+
+@pytest.mark.parametrize("c", [0, 1, 2, 3])
+def test_reprobes_match_oracle(torch_cuda, O, expected, c):
+    inst = synth.load(c)
+    P, Q = both(inst, O)
+    ws = S.workspace([P.handle])
+    bases = reprobe_bases(P.n, P.n_mappings, 500 + c) + [expected[f"config{c}"]["best_index"]]
+    n_swaps = 0
+    for b in bases:
+        say(f"reprobes config {c} base {b}")
+        got = S.sched_eval_reprobes(P.handle, b, ws)
+        want = O.reprobes(Q, b)
+        assert got == want, (c, b)
+        n_swaps += sum(p["kind"] == 2 for p in got)
+    if c == 2:
+        assert n_swaps > 0  # the memory-constrained config exercises swaps
+
+
+def test_reprobes_paper_s13(torch_cuda, O):
+    d = json.load(open(os.path.join(GOLDEN, "paper_scenarios.json")))
+    s = d["scenarios"]["S13"]
+    P = S.Problem(s["tools"], [], d["contention_q16"], s["budget"])
+    Q = O.Problem(s["tools"], [], d["contention_q16"], s["budget"])
+    base = O.index_of(d["s13_whatif"]["base"])
+    got = S.sched_eval_reprobes(P.handle, base, S.workspace([P.handle]))
+    assert got == O.reprobes(Q, base)
+    swaps = {p["swap_tool"]: p for p in got if p["kind"] == 2 and p["tool"] == 2}
+    assert swaps[1]["index"] == 16 and swaps[1]["makespan_us"] == 720903
+    assert swaps[0]["makespan_us"] > swaps[1]["makespan_us"]
+
+
+def test_reprobes_with_measured_latencies(torch_cuda, O):
+    """Re-measured latencies (a batch replica) replace the profiles for the
+    probes only; the problem's own profiles stay in force afterwards."""
+    inst = synth.load(4)
+    sc = inst["scenarios"][3]
+    P = S.Problem.from_instance(sc)
+    ws = S.workspace([P.handle])
+    for r in (0, 17, 63):
+        lat = sc["replicas"][r]
+        Q = O.Problem.from_instance(sc, lat)
+        for b in reprobe_bases(P.n, P.n_mappings, 900 + r):
+            assert S.sched_eval_reprobes(P.handle, b, ws, lat=lat) == O.reprobes(Q, b), (r, b)
+    Q0 = O.Problem.from_instance(sc)
+    assert S.sched_eval_reprobes(P.handle, 5, ws) == O.reprobes(Q0, 5)
+
+
+@pytest.mark.parametrize("n", [2, 20, 40])
+def test_reprobes_wide_and_tight(torch_cuda, O, n):
+    inst = synth.random_instance(7700 + n, n, "permuted", tight=True)
+    P, Q = both(inst, O)
+    ws = S.workspace([P.handle])
+    for b in reprobe_bases(n, P.n_mappings, 40 + n):
+        say(f"reprobes n={n} base {b}")
+        got = S.sched_eval_reprobes(P.handle, b, ws)
+        assert got == O.reprobes(Q, b), (n, b)

@@ -235,6 +235,86 @@ def test_paper_s13_memory_feasibility(oracle_mod):
     assert 656 + 442 <= s["budget"] < 656 + 486 + 442
 
 
+def test_paper_s13_whatif_block(oracle_mod):
+    """Round-3 what-if block of S13 around the round-2 mapping.
+
+    The model gives every printed probe the paper's feasibility, puts the
+    two swaps in the paper's order (C<->B before C<->A) and the single moves
+    to CPU above the base, and the winning swap is the brute-force optimum.
+    The paper measured D->gpu_queue 435 ms below the base; the model, which
+    has no loading overlap, puts it above: a recorded divergence.
+    """
+    O = oracle_mod
+    d = load_paper()
+    s = d["scenarios"]["S13"]
+    w = d["s13_whatif"]
+    P = paper_problem(O, d, s)
+    mem = [t[4] for t in s["tools"]]
+    base = O.index_of(w["base"])
+    probes = O.reprobes(P, base)
+    assert probes[0]["kind"] == 0 and probes[0]["index"] == base
+    by_key = {(p["tool"], p["mode"], p["swap_tool"]): p for p in probes}
+    for e in w["printed"]:
+        p = by_key[(e["tool"], e["mode"], e.get("swap_tool", -1))]
+        assert (p["makespan_us"] < INF) == e["feasible"], e
+        if "full" in e:
+            assert p["index"] == O.index_of(e["full"])
+    # Fan-out: every gpu_now tool starts at 0, so a move is infeasible exactly
+    # when the gpu_now footprints exceed the budget.
+    for p in probes:
+        modes = O.modes_of(p["index"], 4)
+        over = sum(mem[v] for v in range(4) if modes[v] == 1) > s["budget"]
+        assert (p["makespan_us"] == INF) == over, p
+    sw = {e.get("swap_tool"): e for e in w["printed"] if "swap_tool" in e}
+    assert (by_key[(2, 1, 1)]["makespan_us"] < by_key[(2, 1, 0)]["makespan_us"]) == \
+        (sw[1]["e2e_ms"] < sw[0]["e2e_ms"])
+    base_ms = probes[0]["makespan_us"]
+    assert by_key[(1, 0, -1)]["makespan_us"] > by_key[(0, 0, -1)]["makespan_us"] > base_ms
+    assert by_key[(2, 1, 1)]["index"] == P.argmin()[0] == O.index_of(s["paper_oracle"])
+    assert by_key[(3, 2, -1)]["makespan_us"] > base_ms  # divergence, see docstring
+    # Both gpu_now moves that overflow (C and D) get one swap per gpu_now tool.
+    assert [(p["tool"], p["swap_tool"]) for p in probes if p["kind"] == 2] == \
+        [(2, 0), (2, 1), (3, 0), (3, 1)]
+    assert len(probes) == 1 + 2 * 4 + 4
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_reprobe_neighbourhood_by_brute_force(oracle_mod, seed):
+    """The probe set equals its definition checked over every mapping: all
+    mappings one digit away from the base, plus those two digits away that
+    put an overflowing gpu_now move i beside j moved gpu_now -> gpu_queue."""
+    O = oracle_mod
+    n = 5
+    inst = synth.random_instance(9100 + seed, n, "random", tight=True)
+    P = O.Problem(inst["tools"], inst["edges"], inst["contention_q16"], inst["vram_budget_mib"])
+    allms = P.eval_many(range(3 ** n), threads=1)
+    for base in (0, 3 ** n - 1, 121, 40 + 81 * seed % 243, 200):
+        b = O.modes_of(base, n)
+        probes = O.reprobes(P, base)
+        want1, want2 = set(), set()
+        for x in range(3 ** n):
+            m = O.modes_of(x, n)
+            diff = [v for v in range(n) if m[v] != b[v]]
+            if len(diff) == 1:
+                want1.add(x)
+            if len(diff) == 2:
+                for i, j in (diff, diff[::-1]):
+                    mi = list(b)
+                    mi[i] = 1
+                    if (m[i] == 1 and b[j] == 1 and m[j] == 2 and
+                            allms[O.index_of(mi)] == INF):
+                        want2.add(x)
+        got1 = [p["index"] for p in probes if p["kind"] == 1]
+        got2 = [p["index"] for p in probes if p["kind"] == 2]
+        assert sorted(got1) == sorted(want1) and len(got1) == 2 * n
+        assert sorted(set(got2)) == sorted(want2) and len(got2) == len(want2)
+        for p in probes:
+            assert p["makespan_us"] == allms[p["index"]]
+        # order: tool ascending, modes ascending, swaps right after their move
+        keys = [(p["tool"], p["mode"], p["kind"], p["swap_tool"]) for p in probes[1:]]
+        assert keys == sorted(keys)
+
+
 # ---------------------------------------------------------------------------
 # Closed forms and exact alternative computations.
 
