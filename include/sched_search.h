@@ -6,7 +6,11 @@
  * while it runs, an over-budget start is an out-of-memory failure), 2 =
  * gpu_queue (serialized GPU queue, holds no VRAM while waiting, pays load-in).
  * A mapping assigns a mode to every tool; its index is sum_v mode_v * 3^v
- * (tool 0 is the least significant digit).  The library scores mappings with
+ * (tool 0 is the least significant digit).  A problem may restrict each tool
+ * to a subset of the modes (sched_problem_create_masked): then the index is
+ * mixed radix, sum_v digit_v * W_v, where digit_v is the rank of the tool's
+ * mode among its r_v allowed modes (ascending) and W_v = r_0 ... r_(v-1); with
+ * every mode allowed this is the base-3 index above.  The library scores mappings with
  * an integer event-driven schedule (GPU-utilisation contention as a Q16
  * slowdown fixed at each GPU start by the number of co-running GPU tools,
  * VRAM admission, FIFO queue on (ready time, tool), PCIe transfer charged to
@@ -41,10 +45,13 @@ extern "C" {
 #define SCHED_E_SIZE (-2)      /* n_tools not in [1,40], n_levels not in [1,64],
                                   a negative count, n_replicas < 1 */
 #define SCHED_E_VALUE (-3)     /* gpu_us or cpu_us < 1; load, xfer, mem or
-                                  budget < 0; a factor < 65536 or > 2^24 */
+                                  budget < 0; a factor < 65536 or > 2^24; an
+                                  option mask outside [1, 7]; a mode that the
+                                  problem does not allow */
 #define SCHED_E_EDGE (-4)      /* edge endpoint out of range, or a self-loop */
 #define SCHED_E_CYCLE (-5)     /* the edges contain a cycle */
-#define SCHED_E_RANGE (-6)     /* lo >= hi or hi > 3^N; replica map out of range */
+#define SCHED_E_RANGE (-6)     /* lo >= hi or hi > the number of mappings; an
+                                  index beyond it; replica map out of range */
 #define SCHED_E_OVERFLOW (-7)  /* the worst-case makespan bound reaches 2^30 us,
                                   or (N+1)*(budget+1) reaches 2^32: the device
                                   path keeps times and VRAM sums in 32 bits */
@@ -95,9 +102,27 @@ int sched_problem_create(const sched_tool *tools, int32_t n_tools,
                          const uint32_t *contention_q16, int32_t n_levels,
                          int64_t vram_budget_mib, sched_problem **out);
 
+/* The same with a per-tool decision space: allowed[v] (n_tools entries) has
+ * bit m set when tool v may run in mode m (bit 0 cpu, bit 1 gpu_now, bit 2
+ * gpu_queue), each in [1, 7].  Covers the binary GPU/CPU space of S1-S10
+ * (Section 4.1 and Table 3: cpu or gpu_now, 2^N mappings) and tools with no
+ * GPU implementation (the neutral tools of Table 1: cpu only).  A tool with a
+ * single allowed mode takes no digit of the index. */
+int sched_problem_create_masked(const sched_tool *tools, int32_t n_tools,
+                                const sched_edge *edges, int32_t n_edges,
+                                const uint32_t *contention_q16, int32_t n_levels,
+                                int64_t vram_budget_mib, const uint8_t *allowed,
+                                sched_problem **out);
+
 void sched_problem_destroy(sched_problem *p);
 
-/* Number of tools and of mappings (3^N) of a problem. */
+/* Modes of mapping `index` (n_tools entries written to modes), and the index
+ * of per-tool modes (SCHED_E_VALUE if a mode is not allowed).  Host-only. */
+int sched_mapping_modes(const sched_problem *p, uint64_t index, int32_t *modes);
+int sched_mapping_index(const sched_problem *p, const int32_t *modes, uint64_t *index);
+
+/* Number of tools and of mappings (3^N, or the product of the radices) of a
+ * problem. */
 int sched_num_tools(const sched_problem *p, int32_t *out);
 int sched_num_mappings(const sched_problem *p, uint64_t *out);
 
@@ -119,14 +144,15 @@ int sched_bruteforce_argmin(const sched_problem *p, uint64_t lo, uint64_t hi,
  * Section 3.2): replica r is problem replica_problem[r] with the latencies
  * replica_lat[off_r .. off_r + N_r), where off_r is the sum of N over the
  * earlier replicas.  Each replica gets its own exhaustive search over all
- * 3^N mappings; h_out[r] receives its result. */
+ * mappings of its problem; h_out[r] receives its result. */
 int sched_eval_batch(const sched_problem *const *problems, int32_t n_problems,
                      const int32_t *replica_problem, const sched_lat *replica_lat,
                      int32_t n_replicas, void *d_workspace, size_t ws_bytes,
                      void *hip_stream, sched_result *h_out);
 
 /* Score explicit mappings (the what-if probes of Section 3.2): d_idx and
- * d_makespan are device arrays of n entries; each index must be < 3^N.
+ * d_makespan are device arrays of n entries; each index must be below the
+ * number of mappings.
  * d_makespan[i] receives the makespan of d_idx[i] in us, or INT64_MAX when
  * that mapping is infeasible.  Out-of-range indices also yield INT64_MAX. */
 int sched_eval_mappings(const sched_problem *p, const uint64_t *d_idx, int64_t n,
@@ -145,10 +171,11 @@ typedef struct {
 
 /* Bounded what-if exploration around base_index, the runtime monitor's active
  * path (Section 3.2, Algorithm 1): the base mapping first; then for each tool
- * i in order and each other mode a of tool i in the order cpu, gpu_now,
- * gpu_queue, the single-tool move i -> a; right after a move to gpu_now that
- * is infeasible (over the VRAM budget), one swap per tool j on gpu_now in the
- * base mapping (ascending j): i -> gpu_now with j -> gpu_queue.
+ * i in order and each other allowed mode a of tool i in the order cpu,
+ * gpu_now, gpu_queue, the single-tool move i -> a; right after a move to
+ * gpu_now that is infeasible (over the VRAM budget), one swap per tool j on
+ * gpu_now in the base mapping that may use gpu_queue (ascending j):
+ * i -> gpu_now with j -> gpu_queue.
  * lat: optional re-measured latencies (N entries, e.g. running averages) that
  * replace the problem's own for these probes; null keeps the profiles.
  * h_out: host array of capacity entries; capacity must be at least
@@ -156,6 +183,36 @@ typedef struct {
 int sched_eval_reprobes(const sched_problem *p, uint64_t base_index, const sched_lat *lat,
                         void *d_workspace, size_t ws_bytes, void *hip_stream,
                         sched_probe *h_out, int32_t capacity, int32_t *n_out);
+
+/* Sliding-window latency statistics: the runtime monitor's observation
+ * feedback (Section 3.2, Algorithm 1, passive path).  For every tool and mode
+ * the monitor keeps the `window` most recent measured latencies and reports
+ * their running average; re-scoring with those averages in place of the
+ * isolated profiles (sched_eval_batch, sched_eval_reprobes) exposes the
+ * latency the previous mappings actually induced.  Host-only. */
+typedef struct sched_monitor sched_monitor;
+
+/* n_tools in [1, 40], window >= 1. */
+int sched_monitor_create(int32_t n_tools, int32_t window, sched_monitor **out);
+void sched_monitor_destroy(sched_monitor *m);
+
+/* Record one executed round: tool v ran in mode modes[v] (0, 1 or 2) for
+ * latency_us[v] (for gpu_queue, load-in included); a negative latency means
+ * tool v was not observed.  The oldest value of a full window is dropped. */
+int sched_monitor_observe(sched_monitor *m, const int32_t *modes, const int64_t *latency_us);
+
+/* Running averages: for tool v and mode k, entry 3v + k of mean_us gets the
+ * mean of its window rounded half up (0 if empty) and of count the number of
+ * values in it.  Both arrays hold 3 * n_tools entries. */
+int sched_monitor_averages(const sched_monitor *m, int64_t *mean_us, int32_t *count);
+
+/* Latencies for re-scoring (n_tools entries): the profile (n_tools cards)
+ * with every observed quantity replaced by its running average: cpu_us by
+ * the cpu average, gpu_us by the gpu_now average, load_us by the gpu_queue
+ * average minus that gpu_us (at least 0); xfer_us is kept.  An average is
+ * used as a base latency: the schedule model still applies its contention
+ * factor on top. */
+int sched_monitor_latencies(const sched_monitor *m, const sched_tool *profile, sched_lat *out);
 
 /* Static text for an error code. */
 const char *sched_strerror(int code);

@@ -6,6 +6,7 @@ bench's CPU-baseline leg, never by the library or its binding.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 import subprocess
 from typing import Dict, List, Optional, Sequence, Tuple
@@ -146,7 +147,74 @@ def index_of(modes: Sequence[int]) -> int:
     return x
 
 
-def reprobes(P: Problem, base_index: int) -> List[Dict]:
+class Space:
+    """A decision space that allows tool v only the modes in bit mask
+    allowed[v] (bit m for mode m): the binary GPU/CPU space of S1-S10 is mask
+    3 everywhere (Section 4.1, Table 3), a tool with no GPU implementation is
+    mask 1 (Table 1).  A mapping's index is mixed radix: tool v contributes the
+    rank of its mode among its allowed modes times the product of the numbers
+    of allowed modes of tools 0..v-1."""
+
+    def __init__(self, allowed: Sequence[int]):
+        self.options = [[m for m in (CPU, GPU_NOW, GPU_QUEUE) if (int(a) >> m) & 1]
+                        for a in allowed]
+        assert all(self.options), "every tool needs at least one mode"
+        self.n = len(self.options)
+
+    def size(self) -> int:
+        k = 1
+        for o in self.options:
+            k *= len(o)
+        return k
+
+    def modes(self, x: int) -> List[int]:
+        out = []
+        for o in self.options:
+            out.append(o[x % len(o)])
+            x //= len(o)
+        return out
+
+    def index(self, modes: Sequence[int]) -> int:
+        x, w = 0, 1
+        for o, m in zip(self.options, modes):
+            x += o.index(m) * w
+            w *= len(o)
+        return x
+
+    def base3(self, xs: np.ndarray) -> np.ndarray:
+        """Base-3 indices of the mappings with (mixed-radix) indices xs."""
+        xs = np.asarray(xs, dtype=np.uint64).copy()
+        out = np.zeros(len(xs), dtype=np.uint64)
+        p3 = np.uint64(1)
+        for o in self.options:
+            r = np.uint64(len(o))
+            d = xs % r
+            xs //= r
+            out += np.asarray(o, dtype=np.uint64)[d.astype(np.int64)] * p3
+            p3 *= np.uint64(3)
+        return out
+
+
+def masked_argmin(P: Problem, space: Space, chunk: int = 1 << 20, lo: int = 0,
+                  hi: Optional[int] = None) -> Tuple[int, int]:
+    """(index, makespan) of the best mapping of a restricted decision space
+    among indices [lo, hi): the lowest makespan, ties to the lowest index of
+    that space (the exhaustive search of Sections 2.3 and 4.1 over the
+    allowed mappings)."""
+    best = (INFEASIBLE, NO_INDEX)
+    total = space.size() if hi is None else hi
+    for start in range(lo, total, chunk):
+        xs = np.arange(start, min(total, start + chunk), dtype=np.uint64)
+        ms = P.eval_many(space.base3(xs))
+        k = int(np.argmin(ms))  # first minimum: the lowest index of the chunk
+        if (int(ms[k]), start + k) < best:
+            best = (int(ms[k]), start + k)
+    if best[0] == INFEASIBLE:
+        return NO_INDEX, INFEASIBLE
+    return best[1], best[0]
+
+
+def reprobes(P: Problem, base_index: int, space: Optional[Space] = None) -> List[Dict]:
     """Bounded what-if exploration around one mapping (Section 3.2,
     Algorithm 1, the active path run when the mapping changed).
 
@@ -155,18 +223,22 @@ def reprobes(P: Problem, base_index: int) -> List[Dict]:
     move is to gpu_now and it does not fit the VRAM budget (the schedule is
     infeasible), each tool that sits on gpu_now in the base mapping is tried
     in its place on gpu_queue (a swap).  Every probe is scored by the same
-    schedule model as the search, on explicit per-tool modes.
+    schedule model as the search, on explicit per-tool modes.  In a restricted
+    space (Space) only allowed modes are tried, and a swap needs gpu_queue to
+    be allowed to the displaced tool.
     """
-    d = modes_of(base_index, P.n)
+    if space is None:
+        space = Space([7] * P.n)
+    d = space.modes(base_index)
 
     def probe(kind, tool, mode, swap_tool, modes):
-        return {"index": index_of(modes), "makespan_us": P.schedule(modes)[0], "kind": kind,
-                "tool": tool, "mode": mode, "swap_tool": swap_tool}
+        return {"index": space.index(modes), "makespan_us": P.schedule(modes)[0],
+                "kind": kind, "tool": tool, "mode": mode, "swap_tool": swap_tool}
 
     out = [probe(0, -1, -1, -1, d)]
     for i in range(P.n):
         for a in (CPU, GPU_NOW, GPU_QUEUE):
-            if a == d[i]:
+            if a == d[i] or a not in space.options[i]:
                 continue
             moved = list(d)
             moved[i] = a
@@ -174,8 +246,46 @@ def reprobes(P: Problem, base_index: int) -> List[Dict]:
             out.append(r)
             if r["makespan_us"] == INFEASIBLE and a == GPU_NOW:
                 for j in range(P.n):
-                    if d[j] == GPU_NOW:
+                    if d[j] == GPU_NOW and GPU_QUEUE in space.options[j]:
                         swapped = list(moved)
                         swapped[j] = GPU_QUEUE
                         out.append(probe(2, i, GPU_NOW, j, swapped))
     return out
+
+
+class Monitor:
+    """Sliding-window running averages of the runtime monitor's observation
+    feedback (Section 3.2, Algorithm 1, passive path): for every tool and
+    mode, the `window` latest measured latencies and their mean, rounded half
+    up to an integer microsecond."""
+
+    def __init__(self, n: int, window: int):
+        self.n, self.window = n, window
+        self.obs = [[[] for _ in range(3)] for _ in range(n)]
+
+    def observe(self, modes: Sequence[int], latency_us: Sequence[int]) -> None:
+        for v in range(self.n):
+            if latency_us[v] >= 0:
+                w = self.obs[v][modes[v]]
+                w.append(int(latency_us[v]))
+                del w[:-self.window]
+
+    def mean(self, v: int, mode: int) -> Optional[int]:
+        from fractions import Fraction
+        w = self.obs[v][mode]
+        if not w:
+            return None
+        return int(math.floor(Fraction(sum(w), len(w)) + Fraction(1, 2)))
+
+    def latencies(self, profile: Sequence[Sequence[int]]) -> List[List[int]]:
+        """Profile rows with every observed quantity replaced by its average:
+        cpu by the cpu mean, gpu by the gpu_now mean, load by the gpu_queue
+        mean less that gpu latency (never below 0); transfers kept."""
+        out = []
+        for v, (g, c, l, x, _m) in enumerate(profile):
+            mc, mn, mq = self.mean(v, CPU), self.mean(v, GPU_NOW), self.mean(v, GPU_QUEUE)
+            c = c if mc is None else max(1, mc)
+            g = g if mn is None else max(1, mn)
+            l = l if mq is None else max(0, mq - g)
+            out.append([g, c, l, x])
+        return out

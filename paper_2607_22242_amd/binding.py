@@ -23,10 +23,12 @@ ERRORS = {
 NO_INDEX = (1 << 64) - 1
 INFEASIBLE = (1 << 63) - 1
 
-EXPORTED = ["sched_problem_create", "sched_problem_destroy", "sched_num_tools",
+EXPORTED = ["sched_problem_create", "sched_problem_create_masked", "sched_problem_destroy",
+            "sched_mapping_modes", "sched_mapping_index", "sched_num_tools",
             "sched_num_mappings", "sched_workspace_bytes", "sched_bruteforce_argmin",
             "sched_eval_batch", "sched_eval_mappings", "sched_eval_reprobes",
-            "sched_strerror"]
+            "sched_monitor_create", "sched_monitor_destroy", "sched_monitor_observe",
+            "sched_monitor_averages", "sched_monitor_latencies", "sched_strerror"]
 
 
 class sched_tool(ctypes.Structure):
@@ -77,6 +79,14 @@ def lib():
         L.sched_problem_create.argtypes = [P, ctypes.c_int32, P, ctypes.c_int32, P,
                                            ctypes.c_int32, ctypes.c_int64,
                                            ctypes.POINTER(ctypes.c_void_p)]
+        L.sched_problem_create_masked.restype = ctypes.c_int
+        L.sched_problem_create_masked.argtypes = [P, ctypes.c_int32, P, ctypes.c_int32, P,
+                                                  ctypes.c_int32, ctypes.c_int64, P,
+                                                  ctypes.POINTER(ctypes.c_void_p)]
+        L.sched_mapping_modes.restype = ctypes.c_int
+        L.sched_mapping_modes.argtypes = [P, ctypes.c_uint64, P]
+        L.sched_mapping_index.restype = ctypes.c_int
+        L.sched_mapping_index.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint64)]
         L.sched_problem_destroy.restype = None
         L.sched_problem_destroy.argtypes = [P]
         L.sched_num_tools.restype = ctypes.c_int
@@ -97,6 +107,17 @@ def lib():
         L.sched_eval_reprobes.restype = ctypes.c_int
         L.sched_eval_reprobes.argtypes = [P, ctypes.c_uint64, P, P, ctypes.c_size_t, P, P,
                                           ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
+        L.sched_monitor_create.restype = ctypes.c_int
+        L.sched_monitor_create.argtypes = [ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.POINTER(ctypes.c_void_p)]
+        L.sched_monitor_destroy.restype = None
+        L.sched_monitor_destroy.argtypes = [P]
+        L.sched_monitor_observe.restype = ctypes.c_int
+        L.sched_monitor_observe.argtypes = [P, P, P]
+        L.sched_monitor_averages.restype = ctypes.c_int
+        L.sched_monitor_averages.argtypes = [P, P, P]
+        L.sched_monitor_latencies.restype = ctypes.c_int
+        L.sched_monitor_latencies.argtypes = [P, P, P]
         L.sched_strerror.restype = ctypes.c_char_p
         L.sched_strerror.argtypes = [ctypes.c_int]
         _lib = L
@@ -112,19 +133,49 @@ def sched_strerror(code: int) -> str:
     return lib().sched_strerror(code).decode()
 
 
-def sched_problem_create(tools: Sequence[Sequence[int]], edges: Sequence[Sequence[int]],
-                         contention_q16: Sequence[int], vram_budget_mib: int):
-    """Handle (ctypes.c_void_p) of a new problem; tool rows are
-    (gpu_us, cpu_us, load_us, xfer_us, mem_mib)."""
+def _problem_args(tools, edges, contention_q16):
     n = len(tools)
     t = (sched_tool * max(n, 1))(*[sched_tool(*map(int, row)) for row in tools])
     e = (sched_edge * max(len(edges), 1))(*[sched_edge(int(u), int(v)) for u, v in edges])
     f = (ctypes.c_uint32 * max(len(contention_q16), 1))(*map(int, contention_q16))
+    return t, n, (e if len(edges) else None), len(edges), f, len(contention_q16)
+
+
+def sched_problem_create(tools: Sequence[Sequence[int]], edges: Sequence[Sequence[int]],
+                         contention_q16: Sequence[int], vram_budget_mib: int):
+    """Handle (ctypes.c_void_p) of a new problem; tool rows are
+    (gpu_us, cpu_us, load_us, xfer_us, mem_mib)."""
     h = ctypes.c_void_p()
-    rc = lib().sched_problem_create(t, n, e if len(edges) else None, len(edges), f,
-                                    len(contention_q16), int(vram_budget_mib), ctypes.byref(h))
+    rc = lib().sched_problem_create(*_problem_args(tools, edges, contention_q16),
+                                    int(vram_budget_mib), ctypes.byref(h))
     _check(rc, "sched_problem_create")
     return h
+
+
+def sched_problem_create_masked(tools, edges, contention_q16, vram_budget_mib: int,
+                                allowed: Sequence[int]):
+    """As sched_problem_create, with allowed[v] the bit mask of tool v's
+    modes (1 cpu, 2 gpu_now, 4 gpu_queue)."""
+    a = (ctypes.c_uint8 * max(len(allowed), 1))(*map(int, allowed))
+    h = ctypes.c_void_p()
+    rc = lib().sched_problem_create_masked(*_problem_args(tools, edges, contention_q16),
+                                           int(vram_budget_mib), a, ctypes.byref(h))
+    _check(rc, "sched_problem_create_masked")
+    return h
+
+
+def sched_mapping_modes(handle, index: int) -> List[int]:
+    n = sched_num_tools(handle)
+    out = (ctypes.c_int32 * n)()
+    _check(lib().sched_mapping_modes(handle, index, out), "sched_mapping_modes")
+    return list(out)
+
+
+def sched_mapping_index(handle, modes: Sequence[int]) -> int:
+    m = (ctypes.c_int32 * max(len(modes), 1))(*map(int, modes))
+    out = ctypes.c_uint64()
+    _check(lib().sched_mapping_index(handle, m, ctypes.byref(out)), "sched_mapping_index")
+    return out.value
 
 
 def sched_problem_destroy(handle) -> None:
@@ -219,19 +270,87 @@ def sched_eval_reprobes(handle, base_index: int, workspace, lat=None,
             for k in range(got.value)]
 
 
+def sched_monitor_create(n_tools: int, window: int):
+    h = ctypes.c_void_p()
+    _check(lib().sched_monitor_create(n_tools, window, ctypes.byref(h)), "sched_monitor_create")
+    return h
+
+
+def sched_monitor_destroy(handle) -> None:
+    lib().sched_monitor_destroy(handle)
+
+
+def sched_monitor_observe(handle, modes: Sequence[int], latency_us: Sequence[int]) -> None:
+    m = (ctypes.c_int32 * max(len(modes), 1))(*map(int, modes))
+    t = (ctypes.c_int64 * max(len(latency_us), 1))(*map(int, latency_us))
+    _check(lib().sched_monitor_observe(handle, m, t), "sched_monitor_observe")
+
+
+def sched_monitor_averages(handle, n_tools: int) -> Tuple[List[int], List[int]]:
+    """(mean_us, count), each 3 * n_tools long: entry 3v + mode."""
+    mean = (ctypes.c_int64 * (3 * n_tools))()
+    cnt = (ctypes.c_int32 * (3 * n_tools))()
+    _check(lib().sched_monitor_averages(handle, mean, cnt), "sched_monitor_averages")
+    return list(mean), list(cnt)
+
+
+def sched_monitor_latencies(handle, profile: Sequence[Sequence[int]]) -> List[List[int]]:
+    """Rows (gpu_us, cpu_us, load_us, xfer_us) for re-scoring; profile rows
+    are tool cards (gpu_us, cpu_us, load_us, xfer_us, mem_mib)."""
+    n = len(profile)
+    t = (sched_tool * n)(*[sched_tool(*map(int, row)) for row in profile])
+    out = (sched_lat * n)()
+    _check(lib().sched_monitor_latencies(handle, t, out), "sched_monitor_latencies")
+    return [[o.gpu_us, o.cpu_us, o.load_us, o.xfer_us] for o in out]
+
+
+class Monitor:
+    """Owner of a sched_monitor handle (marshalling only)."""
+
+    def __init__(self, n_tools: int, window: int):
+        self.n = n_tools
+        self.handle = sched_monitor_create(n_tools, window)
+
+    def observe(self, modes, latency_us):
+        sched_monitor_observe(self.handle, modes, latency_us)
+
+    def averages(self):
+        return sched_monitor_averages(self.handle, self.n)
+
+    def latencies(self, profile):
+        return sched_monitor_latencies(self.handle, profile)
+
+    def __del__(self):
+        try:
+            if self.handle is not None:
+                sched_monitor_destroy(self.handle)
+                self.handle = None
+        except Exception:
+            pass
+
+
 # ---------------------------------------------------------------------------
 # Convenience owner of a handle (marshalling only).
 
 
 class Problem:
-    def __init__(self, tools, edges, contention_q16, vram_budget_mib):
-        self.handle = sched_problem_create(tools, edges, contention_q16, vram_budget_mib)
+    def __init__(self, tools, edges, contention_q16, vram_budget_mib, allowed=None):
+        if allowed is None:
+            self.handle = sched_problem_create(tools, edges, contention_q16, vram_budget_mib)
+        else:
+            self.handle = sched_problem_create_masked(tools, edges, contention_q16,
+                                                      vram_budget_mib, allowed)
         self.n = sched_num_tools(self.handle)
         self.n_mappings = sched_num_mappings(self.handle)
 
     @classmethod
-    def from_instance(cls, inst):
-        return cls(inst["tools"], inst["edges"], inst["contention_q16"], inst["vram_budget_mib"])
+    def from_instance(cls, inst, allowed=None):
+        """A problem from an instance dict; its "allowed" mode masks, if any,
+        unless `allowed` is given."""
+        if allowed is None:
+            allowed = inst.get("allowed")
+        return cls(inst["tools"], inst["edges"], inst["contention_q16"], inst["vram_budget_mib"],
+                   allowed)
 
     def close(self):
         if self.handle is not None:

@@ -21,6 +21,10 @@ struct sched_problem {
   std::vector<int32_t> order;               // order[i]: original tool with internal label i
   std::vector<int32_t> late;                // tools from the deepest in the DAG to the shallowest
   std::vector<uint32_t> contention;         // F[k-1]
+  std::vector<uint8_t> allowed;             // per tool: bit m set if mode m is allowed
+  std::vector<uint8_t> radix;               // number of allowed modes
+  std::vector<uint64_t> weight;             // W_v: product of the radices of tools < v
+  std::vector<int32_t> enum_tools;          // tools with radix > 1, ascending
   int64_t budget = 0;
   uint64_t n_mappings = 0;
   int32_t n_preds = 0;
@@ -36,10 +40,30 @@ constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 
-uint64_t pow3(int n) {
-  uint64_t m = 1;
-  for (int i = 0; i < n; ++i) m *= 3u;
-  return m;
+// Mode of digit d of tool v (the d-th allowed mode, ascending).
+int mode_of_digit(const sched_problem& p, int v, int d) {
+  for (int m = 0; m < 3; ++m)
+    if ((p.allowed[v] >> m) & 1) {
+      if (d == 0) return m;
+      --d;
+    }
+  return -1;
+}
+
+// Digit of mode m of tool v, or -1 if m is not allowed.
+int digit_of_mode(const sched_problem& p, int v, int m) {
+  if (m < 0 || m > 2 || !((p.allowed[v] >> m) & 1)) return -1;
+  int d = 0;
+  for (int k = 0; k < m; ++k) d += (p.allowed[v] >> k) & 1;
+  return d;
+}
+
+// Options word of tool v's enumeration position: radix, then the mode of
+// each digit.
+uint32_t options_word(const sched_problem& p, int v) {
+  uint32_t o = p.radix[v];
+  for (int d = 0; d < p.radix[v]; ++d) o |= uint32_t(mode_of_digit(p, v, d)) << (2 + 2 * d);
+  return o;
 }
 
 // round(b * f / 2^16), halves up, in 128-bit arithmetic.
@@ -115,12 +139,27 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
     out[kPosBase + v] = uint32_t(i);
     if (tl.mem_mib > budget) big |= 1ull << i;
   }
-  for (int v = 0; v < n; ++v) {  // index order: digit position v is tool v
-    out[kEnumLabBase + v] = uint32_t(label[v]);
-    const uint64_t w = pow3(v);
-    out[kEnumWeightBase + 2 * v] = uint32_t(w);
-    out[kEnumWeightBase + 2 * v + 1] = uint32_t(w >> 32);
+  // Index order: position k holds the k-th tool with a choice; the others
+  // are fixed in the header.
+  uint64_t fix_gn = 0, fix_gq = 0;
+  for (int v = 0; v < n; ++v)
+    if (p.radix[v] == 1) {
+      const int m = mode_of_digit(p, v, 0);
+      if (m == 1) fix_gn |= 1ull << label[v];
+      if (m == 2) fix_gq |= 1ull << label[v];
+    }
+  for (size_t k = 0; k < p.enum_tools.size(); ++k) {
+    const int v = p.enum_tools[k];
+    out[kEnumLabBase + k] = uint32_t(label[v]);
+    out[kEnumWeightBase + 2 * k] = uint32_t(p.weight[v]);
+    out[kEnumWeightBase + 2 * k + 1] = uint32_t(p.weight[v] >> 32);
+    out[kEnumOptBase + k] = options_word(p, v);
   }
+  out[kHdrPositions] = uint32_t(p.enum_tools.size());
+  out[kHdrFixGnLo] = uint32_t(fix_gn);
+  out[kHdrFixGnHi] = uint32_t(fix_gn >> 32);
+  out[kHdrFixGqLo] = uint32_t(fix_gq);
+  out[kHdrFixGqHi] = uint32_t(fix_gq >> 32);
   out[kHdrN] = uint32_t(n);
   out[kHdrLevels] = uint32_t(levels);
   out[kHdrBudget] = uint32_t(budget);
@@ -130,17 +169,57 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
   return SCHED_OK;
 }
 
+// Enumeration order (tools, inner positions first) of a search with J inner
+// digits.  Index order (a partial range): the tools with a choice in
+// ascending number, so that the walk follows the index.  A full range: the
+// four tools deepest in the DAG take the positions right above the J inner
+// digits, so that the lanes of a wave (consecutive outer combinations) differ
+// in tools that act late in every schedule and step through their passes
+// together; the other tools follow from deepest to shallowest.  Any order
+// visits every mapping once.
+std::vector<int32_t> enumeration(const sched_problem& p, bool full, int J) {
+  if (!full) return p.enum_tools;
+  std::vector<int32_t> late;
+  for (int32_t v : p.late)
+    if (p.radix[v] > 1) late.push_back(v);
+  const int P = int(late.size());
+  const int lanes = std::min(4, P - J);
+  std::vector<int32_t> seq;
+  for (int k = 0; k < J; ++k) seq.push_back(late[lanes + k]);
+  for (int k = 0; k < lanes; ++k) seq.push_back(late[k]);
+  for (int k = lanes + J; k < P; ++k) seq.push_back(late[k]);
+  return seq;
+}
+
+// Replicas whose problems share this key share one search plan.
+std::vector<uint8_t> plan_key(const sched_problem& p) {
+  std::vector<uint8_t> k{uint8_t(p.n)};
+  for (int32_t v : p.late)
+    if (p.radix[v] > 1) k.push_back(p.radix[v]);
+  return k;
+}
+
+uint64_t inner_count(const sched_problem& p, const std::vector<int32_t>& seq, int J) {
+  uint64_t c = 1;
+  for (int k = 0; k < J; ++k) c *= p.radix[seq[k]];
+  return c;
+}
+
 // Split [lo, hi) x n_tables into blocks of kBlock lanes; each lane owns one
-// outer combination and enumerates 3^J inner ones.
-void plan_search(int n, uint64_t lo, uint64_t hi, uint32_t n_tables, SearchArgs& a) {
-  const uint64_t span = hi - lo;
-  const unsigned __int128 work = (unsigned __int128)span * n_tables;
+// outer combination and enumerates the inner ones.  J grows while the lanes
+// still number about kTargetLanes.
+void plan_search(const sched_problem& p, uint64_t lo, uint64_t hi, uint32_t n_tables,
+                 SearchArgs& a) {
+  const bool full = lo == 0 && hi == p.n_mappings;
+  const int P = int(p.enum_tools.size());
+  const unsigned __int128 work = (unsigned __int128)(hi - lo) * n_tables;
   int J = 0;
-  uint64_t inner = 1;
-  while (J < kMaxInnerDigits && J < n && (unsigned __int128)inner * 3u * kTargetLanes <= work) {
+  while (J < kMaxInnerDigits && J < P) {
+    const uint64_t next = inner_count(p, enumeration(p, full, J + 1), J + 1);
+    if ((unsigned __int128)next * kTargetLanes > work) break;
     ++J;
-    inner *= 3u;
   }
+  const uint64_t inner = inner_count(p, enumeration(p, full, J), J);
   a.lo = lo;
   a.hi = hi;
   a.inner_digits = uint32_t(J);
@@ -152,27 +231,17 @@ void plan_search(int n, uint64_t lo, uint64_t hi, uint32_t n_tables, SearchArgs&
   const uint64_t cap = std::max<uint64_t>(1, kMaxBlocks / n_tables);
   a.blocks_per_table = uint32_t(std::min<uint64_t>(a.items_per_table, cap));
   a.n_tables = n_tables;
-  a.full_range = (lo == 0 && hi == pow3(n)) ? 1u : 0u;
+  a.full_range = full ? 1u : 0u;
 }
 
-// Enumeration order of a full-range search: the four tools deepest in the
-// DAG take the positions right above the J inner digits, so that the lanes of
-// a wave (consecutive outer combinations) differ in tools that act late in
-// every schedule and step through their passes together; the other tools
-// follow from deepest to shallowest.  Any order visits every mapping once.
-void set_late_enumeration(const sched_problem& p, int J, uint32_t* table) {
-  const int n = p.n;
-  std::vector<int32_t> seq;
-  const int lanes = std::min(4, n - J);
-  for (int k = 0; k < J; ++k) seq.push_back(p.late[lanes + k]);
-  for (int k = 0; k < lanes; ++k) seq.push_back(p.late[k]);
-  for (int k = lanes + J; k < n; ++k) seq.push_back(p.late[k]);
-  for (int pos = 0; pos < n; ++pos) {
-    const int v = seq[pos];
-    table[kEnumLabBase + pos] = table[kPosBase + v];
-    const uint64_t w = pow3(v);
-    table[kEnumWeightBase + 2 * pos] = uint32_t(w);
-    table[kEnumWeightBase + 2 * pos + 1] = uint32_t(w >> 32);
+// Write the enumeration order seq into a table built by build_table.
+void set_enumeration(const sched_problem& p, const std::vector<int32_t>& seq, uint32_t* table) {
+  for (size_t k = 0; k < seq.size(); ++k) {
+    const int v = seq[k];
+    table[kEnumLabBase + k] = table[kPosBase + v];
+    table[kEnumWeightBase + 2 * k] = uint32_t(p.weight[v]);
+    table[kEnumWeightBase + 2 * k + 1] = uint32_t(p.weight[v] >> 32);
+    table[kEnumOptBase + k] = options_word(p, v);
   }
 }
 
@@ -205,13 +274,9 @@ int check_workspace(void* ws, size_t ws_bytes, size_t need) {
     if ((expr) != hipSuccess) return SCHED_E_DEVICE;   \
   } while (0)
 
-}  // namespace
-
-extern "C" {
-
-int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_edge* edges,
-                         int32_t n_edges, const uint32_t* contention_q16, int32_t n_levels,
-                         int64_t vram_budget_mib, sched_problem** out) {
+int create_problem(const sched_tool* tools, int32_t n_tools, const sched_edge* edges,
+                   int32_t n_edges, const uint32_t* contention_q16, int32_t n_levels,
+                   int64_t vram_budget_mib, const uint8_t* allowed, sched_problem** out) {
   if (out == nullptr || tools == nullptr || contention_q16 == nullptr) return SCHED_E_NULL;
   if (n_edges > 0 && edges == nullptr) return SCHED_E_NULL;
   if (n_tools < 1 || n_tools > kMaxTools || n_edges < 0 || n_levels < 1 || n_levels > kMaxLevels)
@@ -224,6 +289,9 @@ int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_e
   }
   for (int32_t l = 0; l < n_levels; ++l)
     if (contention_q16[l] < 65536u || contention_q16[l] > (1u << 24)) return SCHED_E_VALUE;
+  if (allowed != nullptr)
+    for (int32_t v = 0; v < n_tools; ++v)
+      if (allowed[v] < 1 || allowed[v] > 7) return SCHED_E_VALUE;
 
   sched_problem* p = new (std::nothrow) sched_problem;
   if (p == nullptr) return SCHED_E_NOMEM;
@@ -293,7 +361,20 @@ int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_e
       if (depth[a] != depth[b]) return depth[a] > depth[b];
       return n_anc[a] > n_anc[b];
     });
-    p->n_mappings = pow3(n_tools);
+    // Decision space: allowed modes, radices and mixed-radix weights.
+    p->allowed.assign(n_tools, uint8_t(7));
+    if (allowed != nullptr) p->allowed.assign(allowed, allowed + n_tools);
+    p->radix.resize(n_tools);
+    p->weight.resize(n_tools);
+    uint64_t w = 1;
+    for (int32_t v = 0; v < n_tools; ++v) {
+      const uint8_t a = p->allowed[v];
+      p->radix[v] = uint8_t((a & 1) + ((a >> 1) & 1) + ((a >> 2) & 1));
+      p->weight[v] = w;
+      w *= p->radix[v];
+      if (p->radix[v] > 1) p->enum_tools.push_back(v);
+    }
+    p->n_mappings = w;
     p->table_words = table_words(n_tools, total, std::min<int>(n_levels, n_tools));
     p->table.assign(p->table_words, 0u);
     const int rc = build_table(*p, nullptr, p->table.data());
@@ -309,7 +390,51 @@ int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_e
   return SCHED_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_edge* edges,
+                         int32_t n_edges, const uint32_t* contention_q16, int32_t n_levels,
+                         int64_t vram_budget_mib, sched_problem** out) {
+  return create_problem(tools, n_tools, edges, n_edges, contention_q16, n_levels,
+                        vram_budget_mib, nullptr, out);
+}
+
+int sched_problem_create_masked(const sched_tool* tools, int32_t n_tools,
+                                const sched_edge* edges, int32_t n_edges,
+                                const uint32_t* contention_q16, int32_t n_levels,
+                                int64_t vram_budget_mib, const uint8_t* allowed,
+                                sched_problem** out) {
+  if (allowed == nullptr) return SCHED_E_NULL;
+  return create_problem(tools, n_tools, edges, n_edges, contention_q16, n_levels,
+                        vram_budget_mib, allowed, out);
+}
+
 void sched_problem_destroy(sched_problem* p) { delete p; }
+
+int sched_mapping_modes(const sched_problem* p, uint64_t index, int32_t* modes) {
+  if (p == nullptr || modes == nullptr) return SCHED_E_NULL;
+  if (index >= p->n_mappings) return SCHED_E_RANGE;
+  for (int v = 0; v < p->n; ++v) {
+    const int d = int(index % p->radix[v]);
+    index /= p->radix[v];
+    modes[v] = mode_of_digit(*p, v, d);
+  }
+  return SCHED_OK;
+}
+
+int sched_mapping_index(const sched_problem* p, const int32_t* modes, uint64_t* index) {
+  if (p == nullptr || modes == nullptr || index == nullptr) return SCHED_E_NULL;
+  uint64_t x = 0;
+  for (int v = 0; v < p->n; ++v) {
+    const int d = digit_of_mode(*p, v, modes[v]);
+    if (d < 0) return SCHED_E_VALUE;
+    x += uint64_t(d) * p->weight[v];
+  }
+  *index = x;
+  return SCHED_OK;
+}
 
 int sched_num_tools(const sched_problem* p, int32_t* out) {
   if (p == nullptr || out == nullptr) return SCHED_E_NULL;
@@ -353,7 +478,7 @@ int sched_bruteforce_argmin(const sched_problem* p, uint64_t lo, uint64_t hi, vo
   char* ws = static_cast<char*>(d_workspace);
 
   SearchArgs a{};
-  plan_search(p->n, lo, hi, 1, a);
+  plan_search(*p, lo, hi, 1, a);
   a.tables = reinterpret_cast<const uint32_t*>(ws + L.tables);
   a.table_stride = p->table_words;
   a.partials = reinterpret_cast<Partial*>(ws + L.partials);
@@ -365,7 +490,8 @@ int sched_bruteforce_argmin(const sched_problem* p, uint64_t lo, uint64_t hi, vo
   } catch (const std::bad_alloc&) {
     return SCHED_E_NOMEM;
   }
-  if (a.full_range) set_late_enumeration(*p, int(a.inner_digits), table.data());
+  if (a.full_range)
+    set_enumeration(*p, enumeration(*p, true, int(a.inner_digits)), table.data());
   HIP_TRY(hipMemcpyAsync(ws + L.tables, table.data(), size_t(p->table_words) * 4,
                          hipMemcpyHostToDevice, s));
   HIP_TRY(launch_search(p->n, a, s));
@@ -404,11 +530,15 @@ int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
   int rc = check_workspace(d_workspace, ws_bytes, L.total);
   if (rc != SCHED_OK) return rc;
 
-  // Replicas grouped by tool count (one kernel instantiation per count).
+  // Replicas grouped by search plan: tool count (one kernel instantiation
+  // per count) and the radices along the enumeration order, which fix the
+  // inner digits and the outer combinations.
+  std::vector<std::vector<uint8_t>> keys(static_cast<size_t>(n_problems));
+  for (int32_t i = 0; i < n_problems; ++i) keys[size_t(i)] = plan_key(*problems[i]);
   std::vector<int32_t> order(R);
   std::iota(order.begin(), order.end(), 0);
   std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
-    return problems[replica_problem[x]]->n < problems[replica_problem[y]]->n;
+    return keys[size_t(replica_problem[x])] < keys[size_t(replica_problem[y])];
   });
   std::vector<uint32_t> host_tables;
   std::vector<DevResult> host_res;
@@ -425,11 +555,12 @@ int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
   };
   std::vector<Group> groups;
   for (size_t first = 0; first < R;) {
-    const int n = problems[replica_problem[order[first]]]->n;
+    const int32_t pf = replica_problem[order[first]];
     size_t last = first;
-    while (last < R && problems[replica_problem[order[last]]]->n == n) ++last;
+    while (last < R && keys[size_t(replica_problem[order[last]])] == keys[size_t(pf)]) ++last;
     Group g{first, last, SearchArgs{}};
-    plan_search(n, 0, pow3(n), uint32_t(last - first), g.a);
+    const sched_problem& p0 = *problems[pf];
+    plan_search(p0, 0, p0.n_mappings, uint32_t(last - first), g.a);
     // The block cap is shared by the whole batch so partials stay bounded.
     const uint64_t cap = std::max<uint64_t>(1, kMaxBlocks / R);
     g.a.blocks_per_table = uint32_t(std::min<uint64_t>(g.a.items_per_table, cap));
@@ -443,7 +574,7 @@ int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
       uint32_t* tb = host_tables.data() + i * max_stride;
       rc = build_table(p, replica_lat + lat_off[r], tb);
       if (rc != SCHED_OK) return rc;
-      set_late_enumeration(p, int(g.a.inner_digits), tb);
+      set_enumeration(p, enumeration(p, true, int(g.a.inner_digits)), tb);
     }
   }
 
@@ -521,19 +652,15 @@ int sched_eval_reprobes(const sched_problem* p, uint64_t base_index, const sched
   } else {
     table = p->table;
   }
-  // Digits of the base mapping and the weight 3^v of each tool.
-  std::vector<int> d(n);
-  std::vector<uint64_t> w(n);
-  {
-    uint64_t x = base_index, pw = 1;
-    for (int v = 0; v < n; ++v) {
-      d[v] = int(x % 3u);
-      x /= 3u;
-      w[v] = pw;
-      pw *= 3u;
-    }
-  }
-  auto with = [&](uint64_t x, int v, int a) { return x - uint64_t(d[v]) * w[v] + uint64_t(a) * w[v]; };
+  // Modes of the base mapping; moving tool v from mode d[v] to mode a
+  // changes its digit, weighted by W_v.
+  std::vector<int32_t> d(n);
+  sched_mapping_modes(p, base_index, d.data());
+  auto with = [&](uint64_t x, int v, int a) {
+    return x - uint64_t(digit_of_mode(*p, v, d[v])) * p->weight[v] +
+           uint64_t(digit_of_mode(*p, v, a)) * p->weight[v];
+  };
+  auto ok = [&](int v, int a) { return ((p->allowed[v] >> a) & 1) != 0; };
   // Every candidate, in the order of Algorithm 1 (swaps after their move).
   struct Cand {
     int kind, tool, mode, swap_tool;
@@ -543,12 +670,12 @@ int sched_eval_reprobes(const sched_problem* p, uint64_t base_index, const sched
   cands.push_back({0, -1, -1, -1});
   for (int i = 0; i < n; ++i)
     for (int a = 0; a < 3; ++a) {
-      if (a == d[i]) continue;
+      if (a == d[i] || !ok(i, a)) continue;
       idx.push_back(with(base_index, i, a));
       cands.push_back({1, i, a, -1});
       if (a == 1)
         for (int j = 0; j < n; ++j)
-          if (j != i && d[j] == 1) {
+          if (j != i && d[j] == 1 && ok(j, 2)) {
             idx.push_back(with(with(base_index, i, 1), j, 2));
             cands.push_back({2, i, 1, j});
           }

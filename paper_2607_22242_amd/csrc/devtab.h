@@ -8,8 +8,10 @@
 // Tools are stored under internal labels 0..N-1 that follow a topological
 // order of the DAG (every predecessor has a smaller label), so one ascending
 // sweep over the labels sees each tool after all of its predecessors.  The
-// mapping index keeps the caller's tool numbering: digit v of the index is
-// the mode of original tool v, whose internal label is pos[v].
+// mapping index keeps the caller's tool numbering: it is mixed radix, digit v
+// being the rank of original tool v's mode among the r_v modes allowed to it
+// (r_v = 3 when all are), with weight W_v = r_0 r_1 ... r_(v-1).  Tools with a
+// single allowed mode take no digit: their mode is fixed in the header.
 #pragma once
 #include <stdint.h>
 
@@ -29,6 +31,11 @@ enum : uint32_t {
   kHdrBigLo = 3,      // tools whose footprint exceeds the budget (bits 0..31)
   kHdrBigHi = 4,      //                                           (bits 32..63)
   kHdrDurOff = 5,     // word offset of the duration table
+  kHdrPositions = 6,  // P: tools with more than one allowed mode (digit positions)
+  kHdrFixGnLo = 7,    // labels of tools fixed on gpu_now (bits 0..31)
+  kHdrFixGnHi = 8,    //                                   (bits 32..63)
+  kHdrFixGqLo = 9,    // labels of tools fixed on gpu_queue
+  kHdrFixGqHi = 10,
   kHdrWords = 16,
 };
 
@@ -47,14 +54,21 @@ enum : uint32_t {
 
 // pos[v]: internal label of original tool v.
 constexpr uint32_t kPosBase = kHdrWords + kToolWords * kMaxTools;  // 336
-// Enumeration order of a search: digit position p of the enumeration holds
-// the mode of the tool with internal label elab[p], whose weight in the
-// mapping index is ew[p] = 3^(original number) (two words, low first).
-// Positions 0..J-1 are the inner digits, J.. the outer ones.
-constexpr uint32_t kEnumLabBase = kPosBase + kMaxTools;         // 376
-constexpr uint32_t kEnumWeightBase = kEnumLabBase + kMaxTools;  // 416
+// Enumeration order of a search over positions 0..P-1: position p holds the
+// digit of the tool with internal label elab[p], whose weight in the mapping
+// index is ew[p] = W_v of its original number v (two words, low first), and
+// whose options eo[p] give its radix (bits 0-1, 2 or 3) and the mode of
+// digit d in bits 2+2d..3+2d.  Positions 0..J-1 are the inner digits, J.. the
+// outer ones.
+constexpr uint32_t kEnumLabBase = kPosBase + kMaxTools;          // 376
+constexpr uint32_t kEnumWeightBase = kEnumLabBase + kMaxTools;   // 416
+constexpr uint32_t kEnumOptBase = kEnumWeightBase + 2 * kMaxTools;  // 496
 // Predecessor lists (internal labels), then the duration table.
-constexpr uint32_t kPredBase = kEnumWeightBase + 2 * kMaxTools;  // 496
+constexpr uint32_t kPredBase = kEnumOptBase + kMaxTools;  // 536
+
+// Radix and digit -> mode of an enumeration position's options word.
+inline constexpr uint32_t opt_radix(uint32_t o) { return o & 3u; }
+inline constexpr uint32_t opt_mode(uint32_t o, uint32_t d) { return (o >> (2u + 2u * d)) & 3u; }
 
 // Duration table: dur[(i * 2 + q) * levels + (level - 1)] for internal label
 // i, q = 0 for gpu_now (base gpu_us), q = 1 for gpu_queue (gpu_us + load_us).
@@ -79,10 +93,10 @@ struct SearchArgs {
   uint32_t table_stride;
   uint32_t n_tables;
   uint32_t inner_digits;      // J: enumeration positions 0..J-1 are walked per lane
-  uint32_t inner_count;       // 3^J
+  uint32_t inner_count;       // product of the radices of positions 0..J-1
   uint64_t items_per_table;   // ceil(n_outer / kBlock)
   uint32_t blocks_per_table;
-  uint32_t full_range;        // 1: [lo, hi) = [0, 3^N), any enumeration order
+  uint32_t full_range;        // 1: [lo, hi) is every mapping, any enumeration order
 };
 
 struct DevResult {

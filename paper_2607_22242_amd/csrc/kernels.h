@@ -365,36 +365,6 @@ __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict
   return ms;
 }
 
-// Mode masks (internal labels) of tools lo_tool..N-1 of x: x holds their
-// base-3 digits, lowest first, and original tool v maps to label pos[v].
-template <int N>
-__host__ __device__ __forceinline__ void decode_digits(const uint32_t* __restrict__ tab,
-                                                      uint64_t x, int lo_tool, MaskT<N>& gn,
-                                                      MaskT<N>& gq) {
-  using M = MaskT<N>;
-  gn = 0;
-  gq = 0;
-  if (x < (1ull << 32)) {
-    uint32_t y = uint32_t(x);
-    for (int v = lo_tool; v < N; ++v) {
-      const uint32_t q = y / 3u, d = y - 3u * q;
-      const M b = M(1) << tab[kPosBase + v];
-      if (d == 1) gn |= b;
-      if (d == 2) gq |= b;
-      y = q;
-    }
-  } else {
-    for (int v = lo_tool; v < N; ++v) {
-      const uint64_t q = x / 3u;
-      const uint32_t d = uint32_t(x - 3u * q);
-      const M b = M(1) << tab[kPosBase + v];
-      if (d == 1) gn |= b;
-      if (d == 2) gq |= b;
-      x = q;
-    }
-  }
-}
-
 __device__ __forceinline__ void lex_min(uint32_t& ms, uint64_t& x, uint32_t oms, uint64_t ox) {
   if (oms < ms || (oms == ms && ox < x)) {
     ms = oms;
@@ -435,31 +405,29 @@ __device__ __forceinline__ void stage_tables(const uint32_t* tab, uint32_t* lds)
   __syncthreads();
 }
 
-// Mode masks and index weight of enumeration positions [p0, p1) holding
-// the base-3 digits of y (lowest first).
+// Mode masks and index weight of the mapping whose enumeration positions
+// [p0, p1) hold the mixed-radix digits of y (lowest first), together with the
+// tools whose mode is fixed.
 template <int N>
 __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __restrict__ tab,
                                                          uint64_t y, uint32_t p0, uint32_t p1,
                                                          MaskT<N>& gn, MaskT<N>& gq,
                                                          uint64_t& x) {
   using M = MaskT<N>;
-  gn = 0;
-  gq = 0;
+  gn = load_mask<N>(Tab{tab}, kHdrFixGnLo);
+  gq = load_mask<N>(Tab{tab}, kHdrFixGqLo);
   x = 0;
   for (uint32_t p = p0; p < p1; ++p) {
-    const uint64_t q = y / 3u;
-    const uint32_t d = uint32_t(y - 3u * q);
+    const uint32_t o = tab[kEnumOptBase + p];
+    const uint64_t q = opt_radix(o) == 3u ? y / 3u : y >> 1;
+    const uint32_t d = uint32_t(y - uint64_t(opt_radix(o)) * q);
+    const uint32_t m = opt_mode(o, d);
     const M b = M(1) << tab[kEnumLabBase + p];
     const uint64_t w = uint64_t(tab[kEnumWeightBase + 2 * p]) |
                        (uint64_t(tab[kEnumWeightBase + 2 * p + 1]) << 32);
-    if (d == 1) {
-      gn |= b;
-      x += w;
-    }
-    if (d == 2) {
-      gq |= b;
-      x += 2 * w;
-    }
+    if (m == 1u) gn |= b;
+    if (m == 2u) gq |= b;
+    x += uint64_t(d) * w;
     y = q;
   }
 }
@@ -499,7 +467,7 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
   const uint64_t o = a.outer_lo + rel;
   M ogn, ogq;
   uint64_t xo64;  // index weight of the outer digits
-  decode_positions<N>(tab, o, J, N, ogn, ogq, xo64);
+  decode_positions<N>(tab, o, J, tab[kHdrPositions], ogn, ogq, xo64);
   uint32_t ilo = 0, ihi = a.inner_count;
   uint64_t base = 0;
   if constexpr (!FULL) {
@@ -511,8 +479,17 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
   }
   const I xo = I(xo64);
   I bx = I(best_x);
-  M ign = 0, igq = 0;  // inner modes: the same in every lane of the wave
-  I xi = 0;            // index weight of the inner digits
+  // Inner digits (packed 2 bits per position), their modes and their index
+  // weight: the same in every lane of the wave.  All digits start at 0.
+  M ign = 0, igq = 0;
+  uint32_t idig = 0;
+  I xi = 0;
+  for (uint32_t j = 0; j < J; ++j) {
+    const uint32_t m = opt_mode(tab[kEnumOptBase + j], 0u);
+    const M b = M(1) << tab[kEnumLabBase + j];
+    if (m == 1u) ign |= b;
+    if (m == 2u) igq |= b;
+  }
   for (uint32_t i = 0; i < a.inner_count; ++i) {
     if (FULL || (i >= ilo && i < ihi)) {
       const uint32_t ms = evaluate<N>(tab, lds, levels, budget, ogn | ign, ogq | igq, slot);
@@ -533,22 +510,24 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
     }
     // odometer step on the inner digits
     for (uint32_t j = 0; j < J; ++j) {
+      const uint32_t o = tab[kEnumOptBase + j];
+      const uint32_t d = (idig >> (2u * j)) & 3u;
       const M b = M(1) << tab[kEnumLabBase + j];
       const I w = I(uint64_t(tab[kEnumWeightBase + 2 * j]) |
                     (uint64_t(tab[kEnumWeightBase + 2 * j + 1]) << 32));
-      if (igq & b) {  // 2 -> 0, carry
-        igq &= ~b;
-        xi -= 2 * w;
-        continue;
+      ign &= ~b;
+      igq &= ~b;
+      const bool carry = d + 1u == opt_radix(o);
+      const uint32_t m = opt_mode(o, carry ? 0u : d + 1u);
+      if (m == 1u) ign |= b;
+      if (m == 2u) igq |= b;
+      if (!carry) {
+        idig += 1u << (2u * j);
+        xi += w;
+        break;
       }
-      xi += w;
-      if (ign & b) {
-        ign &= ~b;
-        igq |= b;
-      } else {
-        ign |= b;
-      }
-      break;
+      idig &= ~(3u << (2u * j));
+      xi -= I(d) * w;
     }
   }
   if constexpr (FULL) {
@@ -603,7 +582,8 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
     int64_t r = INT64_MAX;
     if (x < n_mappings) {
       M gn, gq;
-      decode_digits<N>(tab, x, 0, gn, gq);
+      uint64_t xw;
+      decode_positions<N>(tab, x, 0, tab[kHdrPositions], gn, gq, xw);
       const uint32_t ms = evaluate<N>(tab, s_lds, levels, budget, gn, gq, &s_wave[threadIdx.x / 64]);
       if (ms != kInf) r = int64_t(ms);
     }

@@ -120,6 +120,34 @@ def test_reprobe_validation_before_any_device_work():
     assert got.value == -7  # nothing written on error
 
 
+def test_masked_problems_on_the_host():
+    c = S.sched_problem_create_masked
+    assert err(c, [TOOL] * 2, [], F, 100, [3, 0]) == "SCHED_E_VALUE"
+    assert err(c, [TOOL] * 2, [], F, 100, [8, 3]) == "SCHED_E_VALUE"
+    L = B.lib()
+    args = B._problem_args([TOOL], [], F)
+    h = ctypes.c_void_p()
+    assert B.ERRORS[L.sched_problem_create_masked(*args, 100, None, ctypes.byref(h))] == \
+        "SCHED_E_NULL"
+    # S1-S10 style: cpu | gpu_now everywhere, one neutral tool on the CPU only
+    P = S.Problem([TOOL] * 5, [[0, 1]], F, 100, [3, 3, 1, 3, 6])
+    assert P.n_mappings == 2 * 2 * 1 * 2 * 2
+    assert S.sched_mapping_modes(P.handle, 0) == [0, 0, 0, 0, 1]
+    assert S.sched_mapping_modes(P.handle, 15) == [1, 1, 0, 1, 2]
+    assert S.sched_mapping_modes(P.handle, 5) == [1, 0, 0, 1, 1]
+    for x in range(P.n_mappings):
+        assert S.sched_mapping_index(P.handle, S.sched_mapping_modes(P.handle, x)) == x
+    assert err(S.sched_mapping_modes, P.handle, 16) == "SCHED_E_RANGE"
+    assert err(S.sched_mapping_index, P.handle, [0, 0, 1, 0, 1]) == "SCHED_E_VALUE"
+    assert err(S.sched_mapping_index, P.handle, [0, 0, 0, 0, 0]) == "SCHED_E_VALUE"
+    # unmasked: base 3, tool 0 least significant
+    Q = S.Problem([TOOL] * 3, [], F, 100)
+    assert S.sched_mapping_modes(Q.handle, 5) == [2, 1, 0]
+    assert S.sched_mapping_index(Q.handle, [2, 1, 0]) == 5
+    R = S.Problem([TOOL] * 40, [], F, 100, [1] * 40)
+    assert R.n_mappings == 1
+
+
 def test_strerror_covers_codes():
     for code, name in B.ERRORS.items():
         assert S.sched_strerror(code) != "unknown error", name

@@ -328,3 +328,153 @@ def test_reprobes_wide_and_tight(torch_cuda, O, n):
         say(f"reprobes n={n} base {b}")
         got = S.sched_eval_reprobes(P.handle, b, ws)
         assert got == O.reprobes(Q, b), (n, b)
+
+
+# ---------------------------------------------------------------------------
+# Restricted decision spaces (per-tool mode masks; the GPU/CPU space).
+
+
+def masked_case(seed):
+    n = 1 + seed % 9
+    inst = synth.random_instance(4400 + seed, n, ["random", "permuted", "fanout", "chain"][seed % 4],
+                                 tight=seed % 2 == 0)
+    rng = np.random.default_rng(5000 + seed)
+    allowed = [int(rng.integers(1, 8)) for _ in range(n)]
+    if seed % 5 == 0:
+        allowed = [3] * n
+    if seed % 7 == 0:
+        allowed[0] = 1
+    return inst, allowed
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_masked_spaces_every_index_search_and_probes(torch_cuda, O, seed):
+    inst, allowed = masked_case(seed)
+    sp = O.Space(allowed)
+    P = S.Problem.from_instance(inst, allowed)
+    Q = O.Problem.from_instance(inst)
+    assert P.n_mappings == sp.size()
+    xs = np.arange(sp.size(), dtype=np.uint64)
+    ref = Q.eval_many(sp.base3(xs))
+    say(f"masked seed {seed} n={P.n} allowed={allowed}")
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, xs), ref)
+    assert gpu_argmin(torch_cuda, P) == O.masked_argmin(Q, sp)
+    rng = np.random.default_rng(seed)
+    for _ in range(3):
+        lo = int(rng.integers(0, sp.size()))
+        hi = int(rng.integers(lo + 1, sp.size() + 1))
+        r = ref[lo:hi]
+        k = int(np.argmin(r))
+        want = (lo + k, int(r[k])) if r[k] != INF64 else (O.NO_INDEX, INF64)
+        assert gpu_argmin(torch_cuda, P, lo, hi) == want, (lo, hi)
+    ws = S.workspace([P.handle])
+    for b in (0, sp.size() - 1, int(rng.integers(0, sp.size()))):
+        assert S.sched_eval_reprobes(P.handle, b, ws) == O.reprobes(Q, b, sp), b
+
+
+def test_masked_batch_mixed_plans(torch_cuda, O):
+    """Problems with the same tool count but different masks in one batch:
+    each replica gets the search of its own space."""
+    insts = [synth.random_instance(4600 + s, 7, "random", tight=True) for s in range(3)]
+    masks = [[7] * 7, [3] * 7, [1, 3, 7, 5, 6, 3, 7]]
+    probs = [S.Problem.from_instance(i, m) for i, m in zip(insts, masks)]
+    rp = [0, 1, 2, 1, 0, 2, 2]
+    lats = [[[max(1, t[0] + 13 * r), max(1, t[1] + 7 * r), t[2], t[3]] for t in insts[pi]["tools"]]
+            for r, pi in enumerate(rp)]
+    handles = [p.handle for p in probs]
+    got = S.sched_eval_batch(handles, rp, lats, S.workspace(handles, len(rp)))
+    for r, pi in enumerate(rp):
+        Q = O.Problem.from_instance(insts[pi], lats[r])
+        assert tuple(got[r]) == O.masked_argmin(Q, O.Space(masks[pi])), r
+
+
+def test_binary_space_paper_scenarios(torch_cuda, O):
+    d = json.load(open(os.path.join(GOLDEN, "paper_scenarios.json")))
+    for name in ["S1", "S2", "S3", "S4", "S5"]:
+        s = d["scenarios"][name]
+        edges = d["diamond_edges"] if s["topology"] == "diamond" else []
+        P = S.Problem(s["tools"], edges, d["contention_q16"], s["budget"], [3, 3, 3, 3])
+        Q = O.Problem(s["tools"], edges, d["contention_q16"], s["budget"])
+        got = gpu_argmin(torch_cuda, P)
+        assert P.n_mappings == 16 and got == O.masked_argmin(Q, O.Space([3, 3, 3, 3]))
+        if name in ("S2", "S4", "S5"):
+            assert S.sched_mapping_modes(P.handle, got[0]) == s["paper_oracle"], name
+
+
+def test_binary_space_of_mixed19(torch_cuda, O):
+    inst = synth.load(3)
+    allowed = [3] * 19
+    for v in inst["neutral_tools"]:
+        allowed[v] = 1
+    P = S.Problem.from_instance(inst, allowed)
+    Q = O.Problem.from_instance(inst)
+    say(f"binary mixed19: {P.n_mappings} mappings")
+    assert gpu_argmin(torch_cuda, P) == O.masked_argmin(Q, O.Space(allowed))
+
+
+def test_binary32_sampled_and_full(torch_cuda, O, expected):
+    inst = synth.load(5)
+    sp = O.Space(inst["allowed"])
+    P = S.Problem.from_instance(inst)
+    Q = O.Problem.from_instance(inst)
+    assert P.n_mappings == sp.size() == 1 << 30
+    rng = np.random.default_rng(55)
+    xs = np.concatenate([rng.integers(0, sp.size(), 100000, dtype=np.uint64),
+                         np.array([0, 1, sp.size() - 1], dtype=np.uint64)])
+    say("binary32 sampled indices")
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, xs), Q.eval_many(sp.base3(xs)))
+    e = expected["config5"]
+    assert e["instance_sha256"] == synth.sha256_of(5)
+    say("binary32 full search")
+    bi, bm = gpu_argmin(torch_cuda, P)
+    assert (bi, bm) == (e["best_index"], e["makespan_us"])
+    assert Q.schedule(sp.modes(bi))[0] == bm
+
+
+def test_masked_wide_problem(torch_cuda, O):
+    inst = synth.random_instance(4700, 40, "permuted", tight=True)
+    allowed = [1] * 20 + [3] * 10 + [5] * 6 + [7] * 4
+    P = S.Problem.from_instance(inst, allowed)
+    Q = O.Problem.from_instance(inst)
+    sp = O.Space(allowed)
+    say(f"masked n=40: {P.n_mappings} mappings")
+    assert gpu_argmin(torch_cuda, P) == O.masked_argmin(Q, sp)
+    rng = np.random.default_rng(40)
+    xs = rng.integers(0, sp.size(), 20000, dtype=np.uint64)
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, xs), Q.eval_many(sp.base3(xs)))
+
+
+def test_monitor_averages_feed_rescoring(torch_cuda, O):
+    """Rounds of observed latencies (schedules of the oracle under perturbed
+    profiles), averaged by the library's sliding window, then used to
+    re-score: the exhaustive search per replica and the what-if probes."""
+    inst = synth.load(4)
+    handles, rp, lats, probs = [], [], [], []
+    rng = np.random.default_rng(31)
+    for si in (0, 6, 12):
+        sc = inst["scenarios"][si]
+        P = S.Problem.from_instance(sc)
+        probs.append(P)
+        handles.append(P.handle)
+        lib, ref = S.Monitor(P.n, 3), O.Monitor(P.n, 3)
+        for r in range(5):
+            world = O.Problem.from_instance(sc, sc["replicas"][r])
+            modes = [int(x) for x in rng.integers(0, 3, P.n)]
+            ms, start, fin = world.schedule(modes)
+            if ms == INF64:
+                continue
+            lat = [f - s for s, f in zip(start, fin)]
+            lib.observe(modes, lat)
+            ref.observe(modes, lat)
+            avg = lib.latencies(sc["tools"])
+            assert avg == ref.latencies(sc["tools"])
+            rp.append(len(probs) - 1)
+            lats.append(avg)
+    got = S.sched_eval_batch(handles, rp, lats, S.workspace(handles, len(rp)))
+    scen = [inst["scenarios"][si] for si in (0, 6, 12)]
+    for k, (pi, lat) in enumerate(zip(rp, lats)):
+        Q = O.Problem.from_instance(scen[pi], lat)
+        assert tuple(got[k]) == Q.argmin(), k
+        ws = S.workspace([probs[pi].handle])
+        assert S.sched_eval_reprobes(probs[pi].handle, got[k][0], ws, lat=lat) == \
+            O.reprobes(Q, got[k][0]), k

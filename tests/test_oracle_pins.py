@@ -315,6 +315,99 @@ def test_reprobe_neighbourhood_by_brute_force(oracle_mod, seed):
         assert keys == sorted(keys)
 
 
+@pytest.mark.parametrize("name", ["S2", "S4", "S5"])
+def test_paper_binary_space_reproduces_table3(oracle_mod, name):
+    """S1-S10 decide GPU or CPU per tool (Section 4.1): 2^4 = 16 mappings.
+    With every tool restricted to cpu or gpu_now, the oracle picks the
+    mapping of Table 3 for S2, S4 and S5."""
+    O = oracle_mod
+    d = load_paper()
+    s = d["scenarios"][name]
+    P = paper_problem(O, d, s)
+    sp = O.Space([3, 3, 3, 3])
+    assert sp.size() == 16
+    x, ms = O.masked_argmin(P, sp)
+    assert sp.modes(x) == s["paper_oracle"]
+    assert ms == P.eval_index(O.index_of(s["paper_oracle"]))
+
+
+def test_paper_binary_space_neutral_tool(oracle_mod):
+    """web_search has no GPU implementation (Table 1).  Restricted to the
+    CPU, S3's optimum agrees with Table 3 on every other tool; S1 stays a
+    recorded divergence (sentiment, see test_paper_known_divergences)."""
+    O = oracle_mod
+    d = load_paper()
+    s = d["scenarios"]["S3"]
+    sp = O.Space([3, 3, 3, 1])
+    assert sp.size() == 8
+    x, _ = O.masked_argmin(paper_problem(O, d, s), sp)
+    assert sp.modes(x)[:3] == s["paper_oracle"][:3] and sp.modes(x)[3] == 0
+    s1 = d["scenarios"]["S1"]
+    x1, _ = O.masked_argmin(paper_problem(O, d, s1), sp)
+    assert sp.modes(x1) != s1["paper_oracle"]
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_masked_space_by_brute_force(oracle_mod, seed):
+    """A restricted space against the full 3^N space: its mappings are the
+    allowed ones, its index order is the colexicographic order of the
+    per-tool ranks, and its optimum is the first allowed mapping of minimum
+    makespan in that order."""
+    O = oracle_mod
+    n = 2 + seed % 5
+    inst = synth.random_instance(9300 + seed, n, ["random", "fanout", "permuted", "chain"][seed % 4],
+                                 tight=seed % 2 == 0)
+    P = O.Problem(inst["tools"], inst["edges"], inst["contention_q16"], inst["vram_budget_mib"])
+    masks = [(seed * 5 + 3 * v) % 7 + 1 for v in range(n)]
+    sp = O.Space(masks)
+    full = P.eval_many(range(3 ** n), threads=1)
+    allowed = []
+    for x in range(3 ** n):
+        m = O.modes_of(x, n)
+        if all((masks[v] >> m[v]) & 1 for v in range(n)):
+            ranks = tuple(bin(masks[v] & ((1 << m[v]) - 1)).count("1") for v in range(n))
+            allowed.append((ranks[::-1], x))
+    allowed.sort()
+    assert len(allowed) == sp.size()
+    for k, (_, x3) in enumerate(allowed):
+        assert int(sp.base3([k])[0]) == x3 and O.index_of(sp.modes(k)) == x3
+        assert sp.index(O.modes_of(x3, n)) == k
+    ms = [full[x3] for _, x3 in allowed]
+    best = min(ms)
+    want = (ms.index(best), best) if best != INF else (O.NO_INDEX, INF)
+    assert O.masked_argmin(P, sp, chunk=7) == want
+    # every mode allowed: the base-3 space itself
+    every = O.Space([7] * n)
+    assert O.masked_argmin(P, every) == P.argmin(threads=1)
+
+
+def test_monitor_running_averages_by_hand(oracle_mod):
+    """Sliding windows worked out by hand (window 3)."""
+    O = oracle_mod
+    M = O.Monitor(3, 3)
+    rounds = [([1, 0, 2], [10, 1, 1000]),
+              ([1, 0, 2], [20, 2, 1400]),
+              ([1, 2, 2], [31, 500, -1]),   # tool 2 not observed
+              ([1, 0, 0], [40, -1, 77])]
+    for modes, lat in rounds:
+        M.observe(modes, lat)
+    assert M.mean(0, 1) == 30        # last three of 10, 20, 31, 40: 91/3 = 30.33
+    assert M.mean(1, 0) == 2         # (1 + 2) / 2 = 1.5, half up
+    assert M.mean(1, 2) == 500
+    assert M.mean(2, 2) == 1200      # (1000 + 1400) / 2
+    assert M.mean(2, 0) == 77
+    assert M.mean(0, 0) is None and M.mean(2, 1) is None
+    profile = [[300, 900, 50, 7, 1], [100, 9, 40, 3, 1], [250, 60, 30, 5, 1]]
+    assert M.latencies(profile) == [
+        [30, 900, 50, 7],            # gpu_now average; cpu and load unobserved
+        [100, 2, 400, 3],            # load = gpu_queue 500 - gpu 100
+        [250, 77, 950, 5],           # load = 1200 - 250 (gpu from the profile)
+    ]
+    M2 = O.Monitor(1, 2)
+    M2.observe([2], [10])
+    assert M2.latencies([[300, 9, 50, 0, 1]]) == [[300, 9, 0, 0]]  # queue faster than gpu: 0
+
+
 # ---------------------------------------------------------------------------
 # Closed forms and exact alternative computations.
 

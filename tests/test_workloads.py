@@ -6,7 +6,7 @@ import pytest
 from workloads import synth
 
 
-@pytest.mark.parametrize("c", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("c", [0, 1, 2, 3, 4, 5])
 def test_committed_instances_regenerate_exactly(c):
     with open(synth.instance_path(c)) as f:
         assert f.read() == synth.dumps(synth.BUILDERS[c]())
@@ -67,6 +67,15 @@ def test_config_shapes():
         assert 0.9 * g - 1 <= c <= 1.1 * g + 1
     for c in range(4):
         assert synth.load(c)["contention_q16"] == [65536, 88474, 117965, 157286]
+
+
+def test_binary_config_shape():
+    c5 = synth.load(5)
+    assert c5["n_tools"] == 32 and acyclic(32, c5["edges"])
+    assert sorted(set(c5["allowed"])) == [1, 3] and c5["allowed"].count(1) == 2
+    assert [v for v in range(32) if c5["allowed"][v] == 1] == c5["neutral_tools"]
+    assert c5["vram_budget_mib"] == sum(t[4] for t in c5["tools"])
+    assert 2 ** c5["allowed"].count(3) == 1 << 30
 
 
 def test_batch_config_shape():

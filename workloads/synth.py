@@ -251,7 +251,33 @@ def config4() -> Dict:
     return {"name": "batch13x64", "n_tools": BATCH_N, "scenarios": scenarios}
 
 
-BUILDERS = {0: config0, 1: config1, 2: config2, 3: config3, 4: config4}
+def config5() -> Dict:
+    """N=32 mixed DAG in the GPU/CPU decision space, 2^30 = 1,073,741,824
+    mappings.
+
+    Scenarios S1-S10 choose GPU or CPU per tool (Section 4.1, Table 3) with no
+    VRAM budget; tools without a GPU implementation run on the CPU only (the
+    neutral tools of Table 1).  Here 30 tools may run on the CPU or on the GPU
+    at once (mode mask 3), two are CPU-only (mask 1), and the budget is the
+    summed footprint, so no mapping runs out of memory.
+    """
+    n = 32
+    rng = SplitMix64(SEED_BASE + 5)
+    tools = [draw_tool(rng) for _ in range(n)]
+    edges = mixed_edges(rng, n, 0.4)
+    pool = list(range(n))
+    neutral = []
+    for _ in range(2):
+        neutral.append(pool.pop(rng.below(len(pool))))
+    for v in neutral:
+        tools[v][1] = max(1, round_half_up(tools[v][0] * rng.uniform_range(0.9, 1.1)))
+    inst = make_instance("binary32", tools, edges, sum(t[4] for t in tools))
+    inst["allowed"] = [1 if v in neutral else 3 for v in range(n)]
+    inst["neutral_tools"] = sorted(neutral)
+    return inst
+
+
+BUILDERS = {0: config0, 1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
 HERE = os.path.dirname(os.path.abspath(__file__))
 INSTANCE_DIR = os.path.join(HERE, "instances")
 
