@@ -184,6 +184,32 @@ int sched_eval_reprobes(const sched_problem *p, uint64_t base_index, const sched
                         void *d_workspace, size_t ws_bytes, void *hip_stream,
                         sched_probe *h_out, int32_t capacity, int32_t *n_out);
 
+/* Counters of one pruned search. */
+typedef struct {
+    uint64_t prefixes;          /* assignments of the prefix tools that were bounded */
+    uint64_t prefixes_searched; /* prefixes whose subspace was searched exhaustively */
+    uint64_t mappings_searched; /* mappings scored by those searches */
+    int64_t initial_bound_us;   /* makespan of the descent's mapping (INT64_MAX if none) */
+    int32_t prefix_tools;       /* tools in the prefix (0: one exhaustive search) */
+    int32_t descent_rounds;     /* neighbourhood evaluations of the descent */
+} sched_prune_stats;
+
+/* Exact search with pruning: the same result as sched_bruteforce_argmin over
+ * every mapping (the lowest makespan, ties to the lowest index), for spaces
+ * too large to enumerate (the problem is NP-hard, Section 2.3).  An upper
+ * bound comes from steepest descent over the what-if neighbourhood of
+ * Algorithm 1 from index 0.  The tools whose modes move the bound most form a
+ * prefix; every prefix assignment gets a lower bound (critical path of the
+ * shortest durations, queued durations summed) and only assignments whose
+ * bound does not exceed the best makespan found so far have their remaining
+ * tools searched exhaustively, most promising first.  Spaces below 2^22
+ * mappings get one exhaustive search.  d_workspace: at least
+ * sched_pruned_workspace_bytes(p) bytes, 256-byte aligned.  stats: optional
+ * counters (host). */
+int sched_pruned_workspace_bytes(const sched_problem *p, size_t *out);
+int sched_pruned_argmin(const sched_problem *p, void *d_workspace, size_t ws_bytes,
+                        void *hip_stream, sched_result *h_out, sched_prune_stats *stats);
+
 /* Sliding-window latency statistics: the runtime monitor's observation
  * feedback (Section 3.2, Algorithm 1, passive path).  For every tool and mode
  * the monitor keeps the `window` most recent measured latencies and reports

@@ -8,5 +8,5 @@ from .binding import (  # noqa: F401
     sched_eval_batch, sched_eval_mappings, sched_eval_reprobes, sched_num_mappings, sched_num_tools,
     sched_mapping_index, sched_mapping_modes, sched_problem_create, sched_problem_create_masked,
     sched_monitor_averages, sched_monitor_create, sched_monitor_destroy, sched_monitor_latencies,
-    sched_monitor_observe, sched_problem_destroy, sched_strerror, sched_workspace_bytes,
-    workspace)
+    sched_monitor_observe, sched_problem_destroy, sched_pruned_argmin,
+    sched_pruned_workspace_bytes, pruned_workspace, sched_strerror, sched_workspace_bytes, workspace)

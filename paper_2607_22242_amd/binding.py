@@ -27,6 +27,7 @@ EXPORTED = ["sched_problem_create", "sched_problem_create_masked", "sched_proble
             "sched_mapping_modes", "sched_mapping_index", "sched_num_tools",
             "sched_num_mappings", "sched_workspace_bytes", "sched_bruteforce_argmin",
             "sched_eval_batch", "sched_eval_mappings", "sched_eval_reprobes",
+            "sched_pruned_workspace_bytes", "sched_pruned_argmin",
             "sched_monitor_create", "sched_monitor_destroy", "sched_monitor_observe",
             "sched_monitor_averages", "sched_monitor_latencies", "sched_strerror"]
 
@@ -54,6 +55,12 @@ class sched_probe(ctypes.Structure):
     _fields_ = [("index", ctypes.c_uint64), ("makespan_us", ctypes.c_int64),
                 ("kind", ctypes.c_int32), ("tool", ctypes.c_int32),
                 ("mode", ctypes.c_int32), ("swap_tool", ctypes.c_int32)]
+
+
+class sched_prune_stats(ctypes.Structure):
+    _fields_ = [("prefixes", ctypes.c_uint64), ("prefixes_searched", ctypes.c_uint64),
+                ("mappings_searched", ctypes.c_uint64), ("initial_bound_us", ctypes.c_int64),
+                ("prefix_tools", ctypes.c_int32), ("descent_rounds", ctypes.c_int32)]
 
 
 class SchedError(RuntimeError):
@@ -107,6 +114,11 @@ def lib():
         L.sched_eval_reprobes.restype = ctypes.c_int
         L.sched_eval_reprobes.argtypes = [P, ctypes.c_uint64, P, P, ctypes.c_size_t, P, P,
                                           ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
+        L.sched_pruned_workspace_bytes.restype = ctypes.c_int
+        L.sched_pruned_workspace_bytes.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+        L.sched_pruned_argmin.restype = ctypes.c_int
+        L.sched_pruned_argmin.argtypes = [P, P, ctypes.c_size_t, P, ctypes.POINTER(sched_result),
+                                          ctypes.POINTER(sched_prune_stats)]
         L.sched_monitor_create.restype = ctypes.c_int
         L.sched_monitor_create.argtypes = [ctypes.c_int32, ctypes.c_int32,
                                            ctypes.POINTER(ctypes.c_void_p)]
@@ -268,6 +280,32 @@ def sched_eval_reprobes(handle, base_index: int, workspace, lat=None,
     return [{"index": out[k].index, "makespan_us": out[k].makespan_us, "kind": out[k].kind,
              "tool": out[k].tool, "mode": out[k].mode, "swap_tool": out[k].swap_tool}
             for k in range(got.value)]
+
+
+def sched_pruned_workspace_bytes(handle) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().sched_pruned_workspace_bytes(handle, ctypes.byref(out)),
+           "sched_pruned_workspace_bytes")
+    return out.value
+
+
+def sched_pruned_argmin(handle, workspace, stream=None) -> Tuple[int, int, dict]:
+    """(best_index, makespan_us, counters) of the exact pruned search."""
+    out = sched_result()
+    st = sched_prune_stats()
+    wp, wb = _ws(workspace)
+    _check(lib().sched_pruned_argmin(handle, wp, wb, _stream_ptr(stream), ctypes.byref(out),
+                                     ctypes.byref(st)), "sched_pruned_argmin")
+    return out.best_index, out.makespan_us, {k: getattr(st, k) for k, _ in st._fields_}
+
+
+def pruned_workspace(handle, device=None):
+    """A 256-byte aligned device workspace for sched_pruned_argmin."""
+    import torch
+    nbytes = sched_pruned_workspace_bytes(handle)
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device or "cuda")
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + nbytes]
 
 
 def sched_monitor_create(n_tools: int, window: int):

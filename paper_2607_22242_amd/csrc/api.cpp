@@ -166,6 +166,25 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
   out[kHdrBigLo] = uint32_t(big);
   out[kHdrBigHi] = uint32_t(big >> 32);
   out[kHdrDurOff] = dur_off;
+  // Bound table: shortest durations per mode and over the allowed modes.
+  const uint32_t bound_off = dur_off + uint32_t(n) * 2u * uint32_t(levels);
+  for (int i = 0; i < n; ++i) {
+    const int v = p.order[i];
+    uint32_t best[3] = {out[kHdrWords + kToolWords * uint32_t(i) + kToolCpu], kInf, kInf};
+    if (!((big >> i) & 1))
+      for (int q = 0; q < 2; ++q)
+        for (int l = 0; l < levels; ++l) {
+          const uint32_t d = out[dur_off + (uint32_t(i) * 2u + uint32_t(q)) * uint32_t(levels) + l];
+          best[1 + q] = std::min(best[1 + q], d);
+        }
+    uint32_t any = kInf;
+    for (int m = 0; m < 3; ++m) {
+      out[bound_off + kBoundWords * uint32_t(i) + m] = best[m];
+      if ((p.allowed[v] >> m) & 1) any = std::min(any, best[m]);
+    }
+    out[bound_off + kBoundWords * uint32_t(i) + 3] = any;
+  }
+  out[kHdrBoundOff] = bound_off;
   return SCHED_OK;
 }
 
@@ -388,6 +407,107 @@ int create_problem(const sched_tool* tools, int32_t n_tools, const sched_edge* e
   }
   *out = p;
   return SCHED_OK;
+}
+
+// One what-if candidate around a base mapping.
+struct Cand {
+  int kind, tool, mode, swap_tool;  // kind 0 base, 1 single-tool move, 2 swap
+};
+
+// The base mapping and its neighbourhood in the order of Algorithm 1: for
+// each tool i and each other allowed mode a, the move i -> a, followed, when
+// a is gpu_now, by one swap per tool j on gpu_now that may use gpu_queue
+// (i -> gpu_now, j -> gpu_queue).  Every swap is listed; callers decide
+// which to keep.
+void neighbourhood(const sched_problem& p, uint64_t base, std::vector<uint64_t>& idx,
+                   std::vector<Cand>& cands) {
+  const int n = p.n;
+  std::vector<int32_t> d(n);
+  sched_mapping_modes(&p, base, d.data());
+  // Moving tool v from mode d[v] to mode a changes its digit, weighted by W_v.
+  auto with = [&](uint64_t x, int v, int a) {
+    return x - uint64_t(digit_of_mode(p, v, d[v])) * p.weight[v] +
+           uint64_t(digit_of_mode(p, v, a)) * p.weight[v];
+  };
+  auto ok = [&](int v, int a) { return ((p.allowed[v] >> a) & 1) != 0; };
+  idx.clear();
+  cands.clear();
+  idx.push_back(base);
+  cands.push_back({0, -1, -1, -1});
+  for (int i = 0; i < n; ++i)
+    for (int a = 0; a < 3; ++a) {
+      if (a == d[i] || !ok(i, a)) continue;
+      idx.push_back(with(base, i, a));
+      cands.push_back({1, i, a, -1});
+      if (a == 1)
+        for (int j = 0; j < n; ++j)
+          if (j != i && d[j] == 1 && ok(j, 2)) {
+            idx.push_back(with(with(base, i, 1), j, 2));
+            cands.push_back({2, i, 1, j});
+          }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Exact search with pruning.
+
+constexpr uint64_t kPruneMinSpace = 1ull << 22;  // smaller spaces: one exhaustive search
+constexpr uint64_t kMaxPrefixes = 1ull << 20;    // bounded prefix assignments per call
+constexpr uint64_t kMinSubspace = 1ull << 12;    // mappings per searched subspace, at least
+constexpr uint32_t kChunkTables = 2048;          // subspaces per search launch
+
+// The prefix: tools with a choice whose shortest durations differ most
+// between their modes come first (their choice moves the bound most), then
+// as many as fit kMaxPrefixes while the subspaces keep kMinSubspace mappings.
+struct PrunePlan {
+  std::vector<int32_t> prefix;  // prefix tools, digit order of the prefix index
+  uint64_t n_prefixes = 1;
+  uint64_t subspace = 1;        // mappings per prefix
+};
+
+PrunePlan plan_prune(const sched_problem& p) {
+  PrunePlan pl;
+  const uint32_t* bt = p.table.data() + p.table[kHdrBoundOff];
+  std::vector<std::pair<uint64_t, int32_t>> spread;
+  for (int32_t v : p.enum_tools) {
+    const uint32_t i = p.table[kPosBase + v];
+    uint32_t lo = kInf, hi = 0;
+    for (int m = 0; m < 3; ++m) {
+      if (!((p.allowed[v] >> m) & 1)) continue;
+      const uint32_t d = bt[kBoundWords * i + m];
+      lo = std::min(lo, d);
+      hi = std::max(hi, d == kInf ? (1u << 30) : d);
+    }
+    spread.push_back({uint64_t(hi - lo), v});
+  }
+  std::stable_sort(spread.begin(), spread.end(),
+                   [](const auto& a, const auto& b) { return a.first > b.first; });
+  pl.subspace = p.n_mappings;
+  for (const auto& sv : spread) {
+    const uint64_t r = p.radix[sv.second];
+    if (pl.n_prefixes * r > kMaxPrefixes || pl.subspace / r < kMinSubspace) break;
+    pl.prefix.push_back(sv.second);
+    pl.n_prefixes *= r;
+    pl.subspace /= r;
+  }
+  return pl;
+}
+
+struct PruneLayout {
+  size_t tables, partials, results, bounds, probe_idx, probe_ms, total;
+};
+
+PruneLayout prune_layout(const sched_problem& p, const PrunePlan& pl) {
+  PruneLayout l;
+  const size_t probes = size_t(1 + 2 * p.n + p.n * (p.n - 1));
+  l.tables = 0;
+  l.partials = align_up(size_t(kChunkTables) * p.table_words * 4);
+  l.results = l.partials + align_up(partial_capacity(kChunkTables) * sizeof(Partial));
+  l.bounds = l.results + align_up(size_t(kChunkTables) * sizeof(DevResult));
+  l.probe_idx = l.bounds + align_up(size_t(pl.n_prefixes) * 4);
+  l.probe_ms = l.probe_idx + align_up(probes * 8);
+  l.total = l.probe_ms + align_up(probes * 8);
+  return l;
 }
 
 }  // namespace
@@ -652,34 +772,12 @@ int sched_eval_reprobes(const sched_problem* p, uint64_t base_index, const sched
   } else {
     table = p->table;
   }
-  // Modes of the base mapping; moving tool v from mode d[v] to mode a
-  // changes its digit, weighted by W_v.
-  std::vector<int32_t> d(n);
-  sched_mapping_modes(p, base_index, d.data());
-  auto with = [&](uint64_t x, int v, int a) {
-    return x - uint64_t(digit_of_mode(*p, v, d[v])) * p->weight[v] +
-           uint64_t(digit_of_mode(*p, v, a)) * p->weight[v];
-  };
-  auto ok = [&](int v, int a) { return ((p->allowed[v] >> a) & 1) != 0; };
-  // Every candidate, in the order of Algorithm 1 (swaps after their move).
-  struct Cand {
-    int kind, tool, mode, swap_tool;
-  };
   std::vector<Cand> cands;
-  idx.push_back(base_index);
-  cands.push_back({0, -1, -1, -1});
-  for (int i = 0; i < n; ++i)
-    for (int a = 0; a < 3; ++a) {
-      if (a == d[i] || !ok(i, a)) continue;
-      idx.push_back(with(base_index, i, a));
-      cands.push_back({1, i, a, -1});
-      if (a == 1)
-        for (int j = 0; j < n; ++j)
-          if (j != i && d[j] == 1 && ok(j, 2)) {
-            idx.push_back(with(with(base_index, i, 1), j, 2));
-            cands.push_back({2, i, 1, j});
-          }
-    }
+  try {
+    neighbourhood(*p, base_index, idx, cands);
+  } catch (const std::bad_alloc&) {
+    return SCHED_E_NOMEM;
+  }
   const size_t m = idx.size();
   ms.assign(m, 0);
   // Scratch for the index list and the makespans: the partials region.
@@ -711,6 +809,189 @@ int sched_eval_reprobes(const sched_problem* p, uint64_t base_index, const sched
     pr.swap_tool = c.swap_tool;
   }
   *n_out = out;
+  return SCHED_OK;
+}
+
+int sched_pruned_workspace_bytes(const sched_problem* p, size_t* out) {
+  if (p == nullptr || out == nullptr) return SCHED_E_NULL;
+  const size_t plain = layout_for(size_t(p->table_words) * 4, partial_capacity(1), 1).total;
+  size_t need = plain;
+  if (p->n_mappings >= kPruneMinSpace) need = std::max(need, prune_layout(*p, plan_prune(*p)).total);
+  *out = need;
+  return SCHED_OK;
+}
+
+int sched_pruned_argmin(const sched_problem* p, void* d_workspace, size_t ws_bytes,
+                        void* hip_stream, sched_result* h_out, sched_prune_stats* stats) {
+  if (p == nullptr || h_out == nullptr) return SCHED_E_NULL;
+  sched_prune_stats st{};
+  if (p->n_mappings < kPruneMinSpace) {  // not worth bounding: one exhaustive search
+    const int rc = sched_bruteforce_argmin(p, 0, p->n_mappings, d_workspace, ws_bytes, hip_stream,
+                                           h_out);
+    if (rc == SCHED_OK && stats != nullptr) {
+      st.prefixes = 1;
+      st.prefixes_searched = 1;
+      st.mappings_searched = p->n_mappings;
+      st.initial_bound_us = INT64_MAX;
+      *stats = st;
+    }
+    return rc;
+  }
+  const int n = p->n;
+  const PrunePlan pl = plan_prune(*p);
+  const PruneLayout L = prune_layout(*p, pl);
+  int rc = check_workspace(d_workspace, ws_bytes, L.total);
+  if (rc != SCHED_OK) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  char* ws = static_cast<char*>(d_workspace);
+  const uint32_t* d_tab = reinterpret_cast<const uint32_t*>(ws + L.tables);
+  const uint32_t stride = p->table_words;
+
+  try {
+    // 1. Upper bound: steepest descent over the what-if neighbourhood of
+    // Algorithm 1 (every single-tool move and swap), from index 0.
+    uint64_t ub_x = 0;
+    int64_t ub_ms = INT64_MAX;
+    {
+      std::vector<uint64_t> idx;
+      std::vector<Cand> cands;
+      std::vector<int64_t> ms;
+      HIP_TRY(hipMemcpyAsync(ws + L.tables, p->table.data(), size_t(stride) * 4,
+                             hipMemcpyHostToDevice, s));
+      uint64_t x = 0;
+      for (int round = 0; round < 4 * n + 4; ++round) {
+        neighbourhood(*p, x, idx, cands);
+        ms.assign(idx.size(), 0);
+        uint64_t* d_idx = reinterpret_cast<uint64_t*>(ws + L.probe_idx);
+        int64_t* d_ms = reinterpret_cast<int64_t*>(ws + L.probe_ms);
+        HIP_TRY(hipMemcpyAsync(d_idx, idx.data(), idx.size() * 8, hipMemcpyHostToDevice, s));
+        HIP_TRY(launch_eval(n, d_tab, d_idx, int64_t(idx.size()), p->n_mappings, d_ms, s));
+        HIP_TRY(hipMemcpyAsync(ms.data(), d_ms, idx.size() * 8, hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        ++st.descent_rounds;
+        size_t best = 0;
+        for (size_t k = 1; k < idx.size(); ++k)
+          if (ms[k] < ms[best] || (ms[k] == ms[best] && idx[k] < idx[best])) best = k;
+        if (ms[best] < ub_ms || (ms[best] == ub_ms && idx[best] < ub_x)) {
+          ub_ms = ms[best];
+          ub_x = idx[best];
+        }
+        if (best == 0) break;  // no neighbour improves on x
+        x = idx[best];
+      }
+    }
+    st.initial_bound_us = ub_ms;
+
+    // 2. Bounds of every prefix assignment.
+    std::vector<uint32_t> btab(p->table);
+    std::vector<int32_t> seq(pl.prefix);
+    for (int32_t v : p->enum_tools)
+      if (std::find(pl.prefix.begin(), pl.prefix.end(), v) == pl.prefix.end()) seq.push_back(v);
+    set_enumeration(*p, seq, btab.data());
+    uint64_t known = 0;
+    for (int32_t v : pl.prefix) known |= 1ull << p->table[kPosBase + v];
+    for (int v = 0; v < n; ++v)
+      if (p->radix[v] == 1) known |= 1ull << p->table[kPosBase + v];
+    HIP_TRY(hipMemcpyAsync(ws + L.tables, btab.data(), size_t(stride) * 4, hipMemcpyHostToDevice,
+                           s));
+    uint32_t* d_bounds = reinterpret_cast<uint32_t*>(ws + L.bounds);
+    HIP_TRY(launch_bound(n, d_tab, uint32_t(pl.prefix.size()), known, int64_t(pl.n_prefixes),
+                         d_bounds, s));
+    std::vector<uint32_t> lb(pl.n_prefixes);
+    HIP_TRY(hipMemcpyAsync(lb.data(), d_bounds, pl.n_prefixes * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    st.prefixes = pl.n_prefixes;
+    st.prefix_tools = int32_t(pl.prefix.size());
+
+    // Survivors: bound <= upper bound (equal bounds may hide a lower index),
+    // most promising first.
+    std::vector<std::pair<uint32_t, uint64_t>> live;
+    for (uint64_t y = 0; y < pl.n_prefixes; ++y)
+      if (lb[y] != kInf && (ub_ms == INT64_MAX || int64_t(lb[y]) <= ub_ms))
+        live.push_back({lb[y], y});
+    std::sort(live.begin(), live.end());
+
+    // 3. Subspaces: the prefix tools fixed, the rest enumerated with the
+    // weights of the full index.
+    sched_problem sub = *p;
+    for (int32_t v : pl.prefix) sub.allowed[v] = uint8_t(1u << mode_of_digit(*p, v, 0));
+    sub.enum_tools.clear();
+    sub.n_mappings = 1;
+    for (int v = 0; v < n; ++v) {
+      const uint8_t a = sub.allowed[v];
+      sub.radix[v] = uint8_t((a & 1) + ((a >> 1) & 1) + ((a >> 2) & 1));
+      if (sub.radix[v] > 1) sub.enum_tools.push_back(v);
+      sub.n_mappings *= sub.radix[v];
+    }
+    std::vector<uint32_t> stab(stride);
+    rc = build_table(sub, nullptr, stab.data());
+    if (rc != SCHED_OK) return rc;
+    const uint64_t fix_gn0 = uint64_t(p->table[kHdrFixGnLo]) | (uint64_t(p->table[kHdrFixGnHi]) << 32);
+    const uint64_t fix_gq0 = uint64_t(p->table[kHdrFixGqLo]) | (uint64_t(p->table[kHdrFixGqHi]) << 32);
+
+    uint64_t best_x = ub_ms == INT64_MAX ? ~0ull : ub_x;
+    int64_t best_ms = ub_ms;
+    std::vector<uint32_t> tables;
+    std::vector<DevResult> res;
+    size_t next = 0;
+    while (next < live.size()) {
+      if (best_ms != INT64_MAX && int64_t(live[next].first) > best_ms) break;
+      size_t end = next;
+      while (end < live.size() && end - next < kChunkTables &&
+             (best_ms == INT64_MAX || int64_t(live[end].first) <= best_ms))
+        ++end;
+      const uint32_t count = uint32_t(end - next);
+      SearchArgs a{};
+      plan_search(sub, 0, sub.n_mappings, count, a);
+      set_enumeration(sub, enumeration(sub, true, int(a.inner_digits)), stab.data());
+      tables.assign(size_t(count) * stride, 0u);
+      for (uint32_t t = 0; t < count; ++t) {
+        uint32_t* tb = tables.data() + size_t(t) * stride;
+        std::copy(stab.begin(), stab.end(), tb);
+        uint64_t y = live[next + t].second, base = 0, gn = fix_gn0, gq = fix_gq0;
+        for (int32_t v : pl.prefix) {
+          const int d = int(y % p->radix[v]);
+          y /= p->radix[v];
+          base += uint64_t(d) * p->weight[v];
+          const int m = mode_of_digit(*p, v, d);
+          const uint64_t b = 1ull << p->table[kPosBase + v];
+          if (m == 1) gn |= b;
+          if (m == 2) gq |= b;
+        }
+        tb[kHdrFixGnLo] = uint32_t(gn);
+        tb[kHdrFixGnHi] = uint32_t(gn >> 32);
+        tb[kHdrFixGqLo] = uint32_t(gq);
+        tb[kHdrFixGqHi] = uint32_t(gq >> 32);
+        tb[kHdrBaseLo] = uint32_t(base);
+        tb[kHdrBaseHi] = uint32_t(base >> 32);
+      }
+      a.tables = d_tab;
+      a.table_stride = stride;
+      a.partials = reinterpret_cast<Partial*>(ws + L.partials);
+      DevResult* d_res = reinterpret_cast<DevResult*>(ws + L.results);
+      HIP_TRY(hipMemcpyAsync(ws + L.tables, tables.data(), tables.size() * 4,
+                             hipMemcpyHostToDevice, s));
+      HIP_TRY(launch_search(n, a, s));
+      HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, count, d_res, s));
+      res.resize(count);
+      HIP_TRY(hipMemcpyAsync(res.data(), d_res, count * sizeof(DevResult), hipMemcpyDeviceToHost,
+                             s));
+      HIP_TRY(hipStreamSynchronize(s));
+      for (const DevResult& r : res)
+        if (r.makespan < best_ms || (r.makespan == best_ms && r.index < best_x)) {
+          best_ms = r.makespan;
+          best_x = r.index;
+        }
+      st.prefixes_searched += count;
+      st.mappings_searched += uint64_t(count) * sub.n_mappings;
+      next = end;
+    }
+    h_out->best_index = best_ms == INT64_MAX ? ~0ull : best_x;
+    h_out->makespan_us = best_ms;
+  } catch (const std::bad_alloc&) {
+    return SCHED_E_NOMEM;
+  }
+  if (stats != nullptr) *stats = st;
   return SCHED_OK;
 }
 

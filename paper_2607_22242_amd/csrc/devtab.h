@@ -36,6 +36,9 @@ enum : uint32_t {
   kHdrFixGnHi = 8,    //                                   (bits 32..63)
   kHdrFixGqLo = 9,    // labels of tools fixed on gpu_queue
   kHdrFixGqHi = 10,
+  kHdrBaseLo = 11,    // index contribution of the fixed tools (a subspace's
+  kHdrBaseHi = 12,    // offset in the mapping index)
+  kHdrBoundOff = 13,  // word offset of the bound table
   kHdrWords = 16,
 };
 
@@ -72,10 +75,17 @@ inline constexpr uint32_t opt_mode(uint32_t o, uint32_t d) { return (o >> (2u + 
 
 // Duration table: dur[(i * 2 + q) * levels + (level - 1)] for internal label
 // i, q = 0 for gpu_now (base gpu_us), q = 1 for gpu_queue (gpu_us + load_us).
+//
+// Bound table (after the duration table): for internal label i, four words
+// bt[4i + m] = the shortest duration tool i can have in mode m (cpu, gpu_now,
+// gpu_queue: the least over contention levels), and bt[4i + 3] = the least
+// of those over the modes the problem allows it; kInf for a GPU mode of a
+// tool whose footprint exceeds the budget (it can never run there).
+constexpr uint32_t kBoundWords = 4;
 
 inline uint32_t table_words(int n, int n_preds, int levels) {
   uint32_t dur_off = kPredBase + ((uint32_t(n_preds) + 3u) & ~3u);
-  return dur_off + uint32_t(n) * 2u * uint32_t(levels);
+  return dur_off + uint32_t(n) * 2u * uint32_t(levels) + kBoundWords * uint32_t(n);
 }
 
 struct Partial {

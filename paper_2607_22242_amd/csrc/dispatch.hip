@@ -16,6 +16,9 @@ hipError_t launch_search_n(const SearchArgs& a, hipStream_t s);
 template <int N>
 hipError_t launch_eval_n(const uint32_t* tab, const uint64_t* idx, int64_t n, uint64_t n_mappings,
                          int64_t* out, hipStream_t s);
+template <int N>
+hipError_t launch_bound_n(const uint32_t* tab, uint32_t K, uint64_t known, int64_t n,
+                          uint32_t* out, hipStream_t s);
 
 __device__ __forceinline__ void lex_min(uint32_t& ms, uint64_t& x, uint32_t oms, uint64_t ox) {
   if (oms < ms || (oms == ms && ox < x)) {
@@ -74,9 +77,16 @@ template <size_t... I>
 static constexpr auto make_eval_table(std::index_sequence<I...>) {
   return std::array<EvalFn, sizeof...(I)>{&launch_eval_n<int(I) + 1>...};
 }
+using BoundFn = hipError_t (*)(const uint32_t*, uint32_t, uint64_t, int64_t, uint32_t*,
+                               hipStream_t);
+template <size_t... I>
+static constexpr auto make_bound_table(std::index_sequence<I...>) {
+  return std::array<BoundFn, sizeof...(I)>{&launch_bound_n<int(I) + 1>...};
+}
 
 static const auto kSearchFns = make_search_table(std::make_index_sequence<kMaxTools>{});
 static const auto kEvalFns = make_eval_table(std::make_index_sequence<kMaxTools>{});
+static const auto kBoundFns = make_bound_table(std::make_index_sequence<kMaxTools>{});
 
 hipError_t launch_search(int n_tools, const SearchArgs& a, hipStream_t s) {
   return kSearchFns[n_tools - 1](a, s);
@@ -85,6 +95,11 @@ hipError_t launch_search(int n_tools, const SearchArgs& a, hipStream_t s) {
 hipError_t launch_eval(int n_tools, const uint32_t* tab, const uint64_t* idx, int64_t n,
                        uint64_t n_mappings, int64_t* out, hipStream_t s) {
   return kEvalFns[n_tools - 1](tab, idx, n, n_mappings, out, s);
+}
+
+hipError_t launch_bound(int n_tools, const uint32_t* tab, uint32_t K, uint64_t known, int64_t n,
+                        uint32_t* out, hipStream_t s) {
+  return kBoundFns[n_tools - 1](tab, K, known, n, out, s);
 }
 
 hipError_t launch_reduce(const Partial* partials, uint32_t per_table, uint32_t n_tables,

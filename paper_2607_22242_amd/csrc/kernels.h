@@ -405,9 +405,9 @@ __device__ __forceinline__ void stage_tables(const uint32_t* tab, uint32_t* lds)
   __syncthreads();
 }
 
-// Mode masks and index weight of the mapping whose enumeration positions
-// [p0, p1) hold the mixed-radix digits of y (lowest first), together with the
-// tools whose mode is fixed.
+// Mode masks and index of the mapping whose enumeration positions [p0, p1)
+// hold the mixed-radix digits of y (lowest first), together with the tools
+// whose mode is fixed (their index contribution is the table's base).
 template <int N>
 __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __restrict__ tab,
                                                          uint64_t y, uint32_t p0, uint32_t p1,
@@ -416,7 +416,7 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
   using M = MaskT<N>;
   gn = load_mask<N>(Tab{tab}, kHdrFixGnLo);
   gq = load_mask<N>(Tab{tab}, kHdrFixGqLo);
-  x = 0;
+  x = uint64_t(tab[kHdrBaseLo]) | (uint64_t(tab[kHdrBaseHi]) << 32);
   for (uint32_t p = p0; p < p1; ++p) {
     const uint32_t o = tab[kEnumOptBase + p];
     const uint64_t q = opt_radix(o) == 3u ? y / 3u : y >> 1;
@@ -591,6 +591,62 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
   }
 }
 
+// Lower bound on the makespan of every mapping that gives the tools in
+// `known` the modes of gn / gq (the others cpu) and leaves the rest free,
+// or kInf if none of them is feasible.  Each tool lasts at least its
+// shortest duration in its mode (any mode allowed to it if free) and starts
+// no earlier than its predecessors end, plus its transfer when both ends
+// are known to sit on different devices; the queued tools run one at a
+// time, so their durations add up.
+template <int N>
+__host__ __device__ __forceinline__ uint32_t prefix_bound(const uint32_t* __restrict__ tab,
+                                                         MaskT<N> gn, MaskT<N> gq,
+                                                         MaskT<N> known) {
+  using M = MaskT<N>;
+  const Tab tp{tab};
+  const uint32_t* bt = tab + tab[kHdrBoundOff];
+  const M gpu = gn | gq;
+  uint32_t C[N];
+  uint32_t lb = 0, qsum = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const bool kn = (known >> i) & 1;
+    const uint32_t mode = ((gn >> i) & 1) ? 1u : (((gq >> i) & 1) ? 2u : 0u);
+    const uint32_t d = bt[kBoundWords * i + (kn ? mode : 3u)];
+    if (d == kInf) return kInf;
+    const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
+    const uint32_t xf = tp[kHdrWords + kToolWords * i + kToolXfer];
+    uint32_t r = 0;
+#pragma unroll
+    for (int u = 0; u < i; ++u) {
+      if ((pm >> u) & 1) {
+        const bool cross = kn && ((known >> u) & 1) && (((gpu >> u) & 1) != ((gpu >> i) & 1));
+        r = umax32(r, C[u] + (cross ? xf : 0u));
+      }
+    }
+    C[i] = r + d;
+    lb = umax32(lb, C[i]);
+    if (kn && mode == 2u) qsum += d;
+  }
+  return umax32(lb, qsum);
+}
+
+// Bounds of prefixes [0, n): prefix y holds the mixed-radix digits of the
+// table's enumeration positions [0, K); known = the labels of those tools
+// and of the tools with a single allowed mode.
+template <int N>
+__global__ __launch_bounds__(kBlock) void bound_kernel(const uint32_t* __restrict__ tab,
+                                                       uint32_t K, uint64_t known, int64_t n,
+                                                       uint32_t* __restrict__ out) {
+  for (int64_t y = int64_t(blockIdx.x) * kBlock + threadIdx.x; y < n;
+       y += int64_t(gridDim.x) * kBlock) {
+    MaskT<N> gn, gq;
+    uint64_t x;
+    decode_positions<N>(tab, uint64_t(y), 0, K, gn, gq, x);
+    out[y] = prefix_bound<N>(tab, gn, gq, MaskT<N>(known));
+  }
+}
+
 // Launchers of one instantiation (explicitly instantiated per tool count in
 // the inst_*.hip translation units).
 template <int N>
@@ -600,6 +656,17 @@ hipError_t launch_search_n(const SearchArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((search_kernel<N, true>), dim3(blocks), dim3(kBlock), 0, s, a);
   else
     hipLaunchKernelGGL((search_kernel<N, false>), dim3(blocks), dim3(kBlock), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int N>
+hipError_t launch_bound_n(const uint32_t* tab, uint32_t K, uint64_t known, int64_t n,
+                          uint32_t* out, hipStream_t s) {
+  int64_t blocks = (n + kBlock - 1) / kBlock;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(bound_kernel<N>, dim3(uint32_t(blocks)), dim3(kBlock), 0, s, tab, K, known,
+                     n, out);
   return hipGetLastError();
 }
 

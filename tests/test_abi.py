@@ -148,6 +148,23 @@ def test_masked_problems_on_the_host():
     assert R.n_mappings == 1
 
 
+def test_pruned_search_validation():
+    P = S.Problem.from_instance(synth.load(2))  # 3^16 mappings: bounded prefixes
+    nbytes = S.sched_pruned_workspace_bytes(P.handle)
+    assert nbytes % 256 == 0 and nbytes > S.sched_workspace_bytes([P.handle])
+    L = B.lib()
+    res = B.sched_result()
+    st = B.sched_prune_stats()
+    call = lambda ws, wb: B.ERRORS[L.sched_pruned_argmin(  # noqa: E731
+        P.handle, ws, wb, None, ctypes.byref(res), ctypes.byref(st))]
+    assert call(256, nbytes - 256) == "SCHED_E_WORKSPACE"
+    assert call(128, nbytes) == "SCHED_E_WORKSPACE"
+    assert B.ERRORS[L.sched_pruned_argmin(P.handle, 256, nbytes, None, None, None)] == \
+        "SCHED_E_NULL"
+    small = S.Problem.from_instance(synth.load(0))
+    assert S.sched_pruned_workspace_bytes(small.handle) == S.sched_workspace_bytes([small.handle])
+
+
 def test_strerror_covers_codes():
     for code, name in B.ERRORS.items():
         assert S.sched_strerror(code) != "unknown error", name

@@ -478,3 +478,64 @@ def test_monitor_averages_feed_rescoring(torch_cuda, O):
         ws = S.workspace([probs[pi].handle])
         assert S.sched_eval_reprobes(probs[pi].handle, got[k][0], ws, lat=lat) == \
             O.reprobes(Q, got[k][0]), k
+
+
+# ---------------------------------------------------------------------------
+# Exact pruned search (branch and bound over a prefix of the tools).
+
+
+def pruned(P):
+    return S.sched_pruned_argmin(P.handle, S.pruned_workspace(P.handle))
+
+
+@pytest.mark.parametrize("c", [1, 2, 3])
+def test_pruned_search_configs(torch_cuda, O, expected, c):
+    P = S.Problem.from_instance(synth.load(c))
+    bi, bm, st = pruned(P)
+    e = expected[f"config{c}"]
+    say(f"pruned config {c}: {st}")
+    assert (bi, bm) == (e["best_index"], e["makespan_us"])
+    assert st["mappings_searched"] <= P.n_mappings
+    if c >= 2:
+        assert st["prefix_tools"] > 0 and st["mappings_searched"] < P.n_mappings // 10
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_pruned_search_random(torch_cuda, O, seed):
+    n = 14 + seed % 2
+    shape = ["random", "permuted", "fanout", "chain"][seed % 4]
+    inst = synth.random_instance(8800 + seed, n, shape, tight=seed % 2 == 0,
+                                 small_values=seed % 5 == 4)
+    P, Q = both(inst, O)
+    bi, bm, st = pruned(P)
+    say(f"pruned seed {seed} n={n} {shape}: {st}")
+    assert (bi, bm) == Q.argmin()
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_pruned_search_masked(torch_cuda, O, seed):
+    n = 23
+    inst = synth.random_instance(9950 + seed, n, ["random", "fanout", "permuted"][seed],
+                                 tight=seed != 1)
+    allowed = [3] * n
+    allowed[seed] = 7
+    allowed[5 + seed] = 1
+    P = S.Problem.from_instance(inst, allowed)
+    Q = O.Problem.from_instance(inst)
+    bi, bm, st = pruned(P)
+    say(f"pruned masked seed {seed}: {P.n_mappings} mappings, {st}")
+    assert (bi, bm) == O.masked_argmin(Q, O.Space(allowed))
+
+
+def test_pruned_search_beyond_the_oracle(torch_cuda, O):
+    """N = 22 (3^22 mappings): the pruned search against the exhaustive
+    kernel, and the oracle re-scores the mapping it returns."""
+    inst = synth.random_instance(9990, 22, "random", tight=True)
+    P, Q = both(inst, O)
+    bi, bm, st = pruned(P)
+    say(f"pruned n=22: {st}")
+    assert st["mappings_searched"] < P.n_mappings // 100
+    assert Q.eval_index(bi) == bm
+    assert st["initial_bound_us"] >= bm
+    say("exhaustive n=22")
+    assert gpu_argmin(torch_cuda, P) == (bi, bm)
