@@ -37,6 +37,16 @@
  *                  tasks left and no such time the mapping is infeasible
  *   makespan = max_v C_v (equal to the max over sinks, Sec. 2.1).
  *
+ * Processor sharing (the other reading of Factor A, selected per problem):
+ * a GPU task's duration is not fixed at its start; every running GPU task
+ * advances at the same rate, 1 / F[min(k, K)] of the isolated speed, with k
+ * recounted at every event.  In integers: a GPU task holds W = b * 2^16 units
+ * of work; while k GPU tasks run, each completes w_k = round(2^32 / F[k])
+ * units per microsecond (halves up); the next GPU finish is t + ceil(R_min /
+ * w_k) for the least remaining work R_min; at the next event every running
+ * GPU task's remaining work drops by (t' - t) * w_k and those at or below 0
+ * finish at t'.  Steps 1-3 and the CPU are as above.
+ *
  * Search: the lowest makespan over an index range [lo, hi), ties to the
  * lowest index; infeasible mappings are never chosen.  Everything is int64.
  */
@@ -59,6 +69,7 @@ typedef struct {
     int64_t contention[OR_MAXLEV]; /* F[k-1] for k = 1..K, Q16 */
     int32_t npred[OR_MAXN];
     int32_t pred[OR_MAXN][OR_MAXN];
+    int32_t sharing; /* 0: fixed at start, 1: processor sharing */
 } or_problem;
 
 int oracle_problem_size(void) { return (int)sizeof(or_problem); }
@@ -212,6 +223,134 @@ int64_t oracle_schedule(const or_problem *P, const int32_t *mode,
     return makespan;
 }
 
+/* Work rate of a GPU task while k GPU tasks run: round(2^32 / F[k]) units of
+ * 2^-16 us per us, halves up. */
+static int64_t ps_rate(const or_problem *P, int k) {
+    int level = k < P->n_levels ? k : P->n_levels;
+    int64_t f = P->contention[level - 1];
+    return (((int64_t)1 << 33) + f) / (2 * f);
+}
+
+/* The same simulation under processor sharing (see the header). */
+int64_t oracle_schedule_ps(const or_problem *P, const int32_t *mode,
+                           int64_t *start_out, int64_t *finish_out) {
+    const int n = P->n;
+    int state[OR_MAXN];
+    int64_t S[OR_MAXN], C[OR_MAXN], r[OR_MAXN], R[OR_MAXN];
+    int preds_done[OR_MAXN], starting[OR_MAXN];
+    int n_done = 0;
+    int64_t t = 0;
+
+    for (int v = 0; v < n; v++) state[v] = WAITING;
+
+    for (;;) {
+        /* 1. release: CPU tasks at their finish, GPU tasks out of work */
+        for (int v = 0; v < n; v++) {
+            if (state[v] != RUNNING) continue;
+            if (on_gpu(mode[v]) ? R[v] <= 0 : C[v] <= t) {
+                state[v] = DONE;
+                C[v] = t;
+                n_done++;
+            }
+        }
+        if (n_done == n) break;
+
+        /* ready times of waiting tasks whose predecessors have all finished */
+        for (int v = 0; v < n; v++) {
+            preds_done[v] = 0;
+            if (state[v] != WAITING) continue;
+            int all = 1;
+            int64_t rv = 0;
+            for (int j = 0; j < P->npred[v]; j++) {
+                int u = P->pred[v][j];
+                if (state[u] != DONE) { all = 0; break; }
+                int64_t arrive = C[u];
+                if (on_gpu(mode[u]) != on_gpu(mode[v])) arrive += P->xfer[v];
+                if (arrive > rv) rv = arrive;
+            }
+            preds_done[v] = all;
+            r[v] = rv;
+        }
+
+        /* 2. immediate starts */
+        int64_t in_use = 0;
+        for (int v = 0; v < n; v++)
+            if (state[v] == RUNNING && on_gpu(mode[v])) in_use += P->mem[v];
+        for (int v = 0; v < n; v++) {
+            starting[v] = 0;
+            if (state[v] == WAITING && mode[v] != OR_GPU_QUEUE && preds_done[v] &&
+                r[v] <= t) {
+                starting[v] = 1;
+                if (mode[v] == OR_GPU_NOW) in_use += P->mem[v];
+            }
+        }
+        if (in_use > P->budget) return OR_INFEASIBLE;
+
+        /* 3. serialized gpu_queue admission, FIFO on (r_v, v) */
+        int queue_busy = 0;
+        for (int v = 0; v < n; v++)
+            if (state[v] == RUNNING && mode[v] == OR_GPU_QUEUE) queue_busy = 1;
+        if (!queue_busy) {
+            int head = -1;
+            for (int v = 0; v < n; v++) {
+                if (state[v] == WAITING && mode[v] == OR_GPU_QUEUE && preds_done[v] &&
+                    r[v] <= t && (head < 0 || r[v] < r[head]))
+                    head = v;
+            }
+            if (head >= 0 && P->mem[head] <= P->budget - in_use) {
+                starting[head] = 1;
+                in_use += P->mem[head];
+            }
+        }
+
+        /* 4. starts: CPU finish times fixed, GPU tasks take their work */
+        for (int v = 0; v < n; v++) {
+            if (!starting[v]) continue;
+            state[v] = RUNNING;
+            S[v] = t;
+            if (mode[v] == OR_CPU) C[v] = t + P->cpu[v];
+            else R[v] = base_latency(P, v, mode[v]) << 16;
+        }
+
+        /* 5. next event, at the rate of the GPU tasks running from t on */
+        int k = 0;
+        int64_t rmin = 0;
+        for (int v = 0; v < n; v++)
+            if (state[v] == RUNNING && on_gpu(mode[v])) {
+                if (k == 0 || R[v] < rmin) rmin = R[v];
+                k++;
+            }
+        int64_t w = k ? ps_rate(P, k) : 0;
+        int64_t next = OR_INFEASIBLE;
+        if (k) next = t + (rmin + w - 1) / w;
+        for (int v = 0; v < n; v++) {
+            if (state[v] == RUNNING && !on_gpu(mode[v]) && C[v] > t && C[v] < next) next = C[v];
+            if (state[v] == WAITING && preds_done[v] && r[v] > t && r[v] < next) next = r[v];
+        }
+        if (next == OR_INFEASIBLE) return OR_INFEASIBLE; /* a queued task never fits */
+        for (int v = 0; v < n; v++)
+            if (state[v] == RUNNING && on_gpu(mode[v])) R[v] -= (next - t) * w;
+        t = next;
+    }
+
+    int64_t makespan = 0;
+    for (int v = 0; v < n; v++) {
+        if (C[v] > makespan) makespan = C[v];
+        if (start_out) start_out[v] = S[v];
+        if (finish_out) finish_out[v] = C[v];
+    }
+    return makespan;
+}
+
+void oracle_set_sharing(or_problem *P, int32_t sharing) { P->sharing = sharing ? 1 : 0; }
+
+/* Simulate one mapping under the problem's contention reading. */
+int64_t oracle_simulate(const or_problem *P, const int32_t *mode, int64_t *start_out,
+                        int64_t *finish_out) {
+    if (P->sharing) return oracle_schedule_ps(P, mode, start_out, finish_out);
+    return oracle_schedule(P, mode, start_out, finish_out);
+}
+
 /* Mode of every tool for mapping index x: digit v of x in base 3. */
 static void decode_index(int n, uint64_t x, int32_t *mode) {
     for (int v = 0; v < n; v++) {
@@ -223,7 +362,7 @@ static void decode_index(int n, uint64_t x, int32_t *mode) {
 int64_t oracle_eval_index(const or_problem *P, uint64_t x) {
     int32_t mode[OR_MAXN];
     decode_index(P->n, x, mode);
-    return oracle_schedule(P, mode, 0, 0);
+    return oracle_simulate(P, mode, 0, 0);
 }
 
 uint64_t oracle_num_mappings(const or_problem *P) {

@@ -46,6 +46,11 @@ def lib():
         L.oracle_problem_init.argtypes = [
             ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
             ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64]
+        L.oracle_set_sharing.restype = None
+        L.oracle_set_sharing.argtypes = [ctypes.c_void_p, ctypes.c_int32]
+        L.oracle_simulate.restype = ctypes.c_int64
+        L.oracle_simulate.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_void_p]
         L.oracle_schedule.restype = ctypes.c_int64
         L.oracle_schedule.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_void_p]
@@ -75,7 +80,7 @@ class Problem:
     """One scheduling instance held in the oracle's own C struct."""
 
     def __init__(self, tools: Sequence[Sequence[int]], edges: Sequence[Sequence[int]],
-                 contention_q16: Sequence[int], vram_budget_mib: int):
+                 contention_q16: Sequence[int], vram_budget_mib: int, sharing: bool = False):
         L = lib()
         self.n = len(tools)
         self._buf = ctypes.create_string_buffer(L.oracle_problem_size())
@@ -86,13 +91,17 @@ class Problem:
                                    len(f), f.ctypes.data, int(vram_budget_mib))
         if rc != 0:
             raise ValueError("oracle: bad problem")
+        L.oracle_set_sharing(self._buf, 1 if sharing else 0)
+        self.sharing = bool(sharing)
 
     @classmethod
-    def from_instance(cls, inst: Dict, replica_lat: Optional[Sequence[Sequence[int]]] = None):
+    def from_instance(cls, inst: Dict, replica_lat: Optional[Sequence[Sequence[int]]] = None,
+                      sharing: bool = False):
         tools = [list(t) for t in inst["tools"]]
         if replica_lat is not None:
             tools = [list(l[:4]) + [t[4]] for l, t in zip(replica_lat, tools)]
-        return cls(tools, inst["edges"], inst["contention_q16"], inst["vram_budget_mib"])
+        return cls(tools, inst["edges"], inst["contention_q16"], inst["vram_budget_mib"],
+                   sharing)
 
     @property
     def ptr(self):
@@ -107,7 +116,7 @@ class Problem:
         assert len(m) == self.n
         s = np.zeros(self.n, dtype=np.int64)
         c = np.zeros(self.n, dtype=np.int64)
-        ms = lib().oracle_schedule(self.ptr, m.ctypes.data, s.ctypes.data, c.ctypes.data)
+        ms = lib().oracle_simulate(self.ptr, m.ctypes.data, s.ctypes.data, c.ctypes.data)
         return int(ms), s.tolist(), c.tolist()
 
     def eval_index(self, x: int) -> int:

@@ -596,6 +596,135 @@ def test_event_simulation_matches_tick_simulation(oracle_mod, seed, shape, tight
         assert got[x] == want, (seed, x)
 
 
+# Processor sharing (the other reading of Factor A).
+
+
+def ps_rate(f):
+    return ((1 << 33) + f) // (2 * f)  # round(2^32 / f), halves up
+
+
+def ps_tick_simulate(tools, edges, table, budget, modes, horizon=20000):
+    """Processor sharing advanced one microsecond at a time: each tick every
+    running GPU task completes ps_rate(F[k]) units of its b * 2^16 units of
+    work, and finishes at the first tick where none is left."""
+    n = len(tools)
+    preds = [[] for _ in range(n)]
+    for u, v in edges:
+        if u not in preds[v]:
+            preds[v].append(u)
+    state = ["wait"] * n
+    fin = [0] * n
+    rem = [0] * n
+    on_gpu = [m != 0 for m in modes]
+    for t in range(horizon):
+        for v in range(n):
+            if state[v] == "run" and (rem[v] <= 0 if on_gpu[v] else fin[v] <= t):
+                state[v] = "done"
+                fin[v] = t
+        if all(s == "done" for s in state):
+            return max(fin)
+        ready = {}
+        for v in range(n):
+            if state[v] == "wait" and all(state[u] == "done" for u in preds[v]):
+                ready[v] = max([fin[u] + (tools[v][3] if on_gpu[u] != on_gpu[v] else 0)
+                                for u in preds[v]] + [0])
+        used = sum(tools[v][4] for v in range(n) if state[v] == "run" and on_gpu[v])
+        starters = [v for v in sorted(ready) if modes[v] != 2 and ready[v] <= t]
+        used += sum(tools[v][4] for v in starters if modes[v] == 1)
+        if used > budget:
+            return INF
+        if not any(state[v] == "run" and modes[v] == 2 for v in range(n)):
+            queued = sorted((ready[v], v) for v in ready if modes[v] == 2 and ready[v] <= t)
+            if queued and tools[queued[0][1]][4] <= budget - used:
+                starters.append(queued[0][1])
+        for v in starters:
+            g, c, l, x, m = tools[v]
+            state[v] = "run"
+            if modes[v] == 0:
+                fin[v] = t + c
+            else:
+                rem[v] = (g if modes[v] == 1 else g + l) << 16
+        k = sum(1 for v in range(n) if on_gpu[v] and state[v] == "run")
+        if k:
+            w = ps_rate(table[min(k, len(table)) - 1])
+            for v in range(n):
+                if on_gpu[v] and state[v] == "run":
+                    rem[v] -= w
+    return INF
+
+
+def test_ps_hand_cases(oracle_mod):
+    O = oracle_mod
+    # V4 under processor sharing: t1 ends at 150 (100 at 1.5x) having let t0
+    # do 100 of its 400; t0 runs alone for the other 300.
+    P = mk(O, [[400, 5000, 50, 0, 1], [100, 5000, 50, 0, 1]], [], 16)
+    Ps = O.Problem([[400, 5000, 50, 0, 1], [100, 5000, 50, 0, 1]], [], F2, 16, sharing=True)
+    assert P.eval_index(4) == 600 and Ps.eval_index(4) == 450
+    # one GPU task at 1.0x: exactly its latency; a lone queued task pays load
+    one = O.Problem([[123, 9000, 45, 0, 1]], [], F2, 16, sharing=True)
+    assert [one.eval_index(x) for x in range(3)] == [9000, 123, 168]
+    assert ps_rate(65536) == 65536 and ps_rate(98304) == 43691
+
+
+@pytest.mark.parametrize("seed,shape,tight", [
+    (0, "random", False), (1, "random", True), (2, "fanout", True),
+    (3, "chain", False), (4, "random", True), (5, "fanout", False)])
+def test_ps_event_simulation_matches_tick_simulation(oracle_mod, seed, shape, tight):
+    O = oracle_mod
+    n = 4
+    inst = synth.random_instance(700 + seed, n, shape, levels=3, tight=tight,
+                                 small_values=True)
+    P = O.Problem.from_instance(inst, sharing=True)
+    got = P.eval_many(range(3 ** n), threads=1)
+    for x in range(3 ** n):
+        want = ps_tick_simulate(inst["tools"], inst["edges"], inst["contention_q16"],
+                                inst["vram_budget_mib"], O.modes_of(x, n))
+        assert got[x] == want, (seed, x)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_ps_fanout_against_exact_sharing(oracle_mod, seed):
+    """All-gpu_now fan-outs against processor sharing in exact rationals:
+    tasks finish in order of work; while k run each advances at 1 / F[k].
+    The integer reading stays within one microsecond per event plus the
+    rounding of the rates."""
+    from fractions import Fraction
+    O = oracle_mod
+    n = 3 + seed % 4
+    inst = synth.random_instance(800 + seed, n, "fanout", levels=4)
+    F = inst["contention_q16"]
+    P = O.Problem(inst["tools"], [], F, sum(t[4] for t in inst["tools"]), sharing=True)
+    work = sorted(t[0] for t in inst["tools"])
+    t, done = Fraction(0), 0
+    for i, wv in enumerate(work):
+        k = n - i
+        t += (wv - done) * Fraction(F[min(k, len(F)) - 1], 1 << 16)
+        done = wv
+    got = P.eval_index(O.index_of([1] * n))
+    rel = max(Fraction(1, 2 * ps_rate(f)) for f in F)
+    assert abs(got - t) <= n + 1 + t * rel * 2
+
+
+def test_paper_ps_readings(oracle_mod):
+    """Processor sharing picks Table 3's mapping for S1, which the
+    fixed-at-start reading misses, but makes all-GPU win S5 (613.8 ms, worked
+    out by hand in the exact reading) where the paper offloads C."""
+    O = oracle_mod
+    d = load_paper()
+    sp = O.Space([3, 3, 3, 3])
+    s1 = d["scenarios"]["S1"]
+    P1 = O.Problem(s1["tools"], d["diamond_edges"], d["contention_q16"], s1["budget"],
+                   sharing=True)
+    assert sp.modes(O.masked_argmin(P1, sp)[0]) == s1["paper_oracle"]
+    s5 = d["scenarios"]["S5"]
+    P5 = O.Problem(s5["tools"], [], d["contention_q16"], s5["budget"], sharing=True)
+    x, ms = O.masked_argmin(P5, sp)
+    assert sp.modes(x) == [1, 1, 1, 1] != s5["paper_oracle"]
+    # B ends at 136 * 2.4 = 326.4 ms, D 9 ms of work later at 1.8x (342.6),
+    # C 132 ms of work later at 1.35x (520.8), A its last 93 ms alone.
+    assert abs(ms - 613800) <= 4
+
+
 # ---------------------------------------------------------------------------
 # Invariants of returned schedules.
 
