@@ -6,11 +6,15 @@ schedule evaluation and (makespan, index) argmin, all in the HIP library.
 Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps 5] [--warmup 1] [--no-cpu-baseline]
-                    [--config 0..5]
+                    [--config 0..5] [--sharing] [--mode search|pruned|reprobes]
 
 --config selects another synthetic workload for the same measurement: 0-2 a
 single search, 4 one batched call (13 scenarios x 64 replicas x 3^14), 5 a
 single search of a 32-tool DAG in the GPU/CPU space (2^30 mappings).
+--sharing scores mappings under processor-sharing contention instead of the
+fixed-at-start reading.  --mode pruned times the exact pruned search (value:
+mappings of the whole space per second); --mode reprobes times one what-if
+exploration around the optimum (value: probes per second).
 """
 from __future__ import annotations
 
@@ -93,6 +97,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--config", type=int, default=HEADLINE_CONFIG, choices=range(6))
+    ap.add_argument("--sharing", action="store_true")
+    ap.add_argument("--mode", default="search", choices=["search", "pruned", "reprobes"])
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only run one plain device-to-device copy of this many MiB "
                          "(the reference kernel for scaling HBM byte counters)")
@@ -119,9 +125,25 @@ def main():
 
     inst = synth.load(args.config)
     stream = torch.cuda.current_stream()
-    if args.config == 4:
+    extra = {}
+    if args.mode != "search":
+        if args.config == 4:
+            sys.exit("--mode pruned / reprobes take a single-problem config")
+        P = S.Problem.from_instance(inst, sharing=args.sharing)
+        n_tools, n_edges = P.n, len(inst["edges"])
+        if args.mode == "pruned":
+            ws = S.pruned_workspace(P.handle)
+            total = P.n_mappings
+            run = lambda: S.sched_pruned_argmin(P.handle, ws, stream)  # noqa: E731
+        else:
+            ws = S.workspace([P.handle])
+            best = S.sched_bruteforce_argmin(P.handle, 0, P.n_mappings, ws, stream)[0]
+            probes = len(S.sched_eval_reprobes(P.handle, best, ws, stream=stream))
+            total = probes
+            run = lambda: S.sched_eval_reprobes(P.handle, best, ws, stream=stream)  # noqa: E731
+    elif args.config == 4:
         scen = inst["scenarios"]
-        problems = [S.Problem.from_instance(sc) for sc in scen]
+        problems = [S.Problem.from_instance(sc, sharing=args.sharing) for sc in scen]
         handles = [p.handle for p in problems]
         rp = [si for si, sc in enumerate(scen) for _ in sc["replicas"]]
         lat = [rep for sc in scen for rep in sc["replicas"]]
@@ -131,7 +153,7 @@ def main():
         n_edges = sum(len(sc["edges"]) for sc in scen) / len(scen)
         run = lambda: S.sched_eval_batch(handles, rp, lat, ws, stream)  # noqa: E731
     else:
-        P = S.Problem.from_instance(inst)
+        P = S.Problem.from_instance(inst, sharing=args.sharing)
         ws = S.workspace([P.handle])
         total = P.n_mappings
         n_tools, n_edges = P.n, len(inst["edges"])
@@ -160,10 +182,18 @@ def main():
 
     exp_path = os.path.join(ROOT, "tests", "golden", "expected_configs.json")
     expected = None
-    if os.path.exists(exp_path):
+    if os.path.exists(exp_path) and not args.sharing:
         with open(exp_path) as f:
             expected = json.load(f).get(f"config{args.config}")
-    if args.config == 4:
+    if args.mode == "pruned":
+        check = {"best_index": result[0], "makespan_us": result[1]}
+        extra = {"pruned": result[2]}
+        if expected:
+            check["matches_oracle"] = (result[0] == expected["best_index"] and
+                                       result[1] == expected["makespan_us"])
+    elif args.mode == "reprobes":
+        check = {"probes": len(result)}
+    elif args.config == 4:
         check = {"replicas": len(result)}
         if expected:
             want = [tuple(x) for row in expected["results"] for x in row]
@@ -185,10 +215,20 @@ def main():
         5: "binary32: 32-tool random DAG (24 edges) in the GPU/CPU space, 2 CPU-only tools, "
            "2^30 mappings, no VRAM limit",
     }
+    unit = {"search": "mappings/s", "pruned": "mappings/s (whole space, pruned search)",
+            "reprobes": "probes/s"}[args.mode]
+    roofline = {"bound": "alu", "achieved": achieved / 1e12,
+                "peak": VALU_PEAK_OPS / 1e12, "unit": "Tops/s (int32 VALU lane-ops)",
+                "frac": achieved / VALU_PEAK_OPS,
+                "traffic": (TRAFFIC_BYTES if args.config == HEADLINE_CONFIG and not args.sharing
+                            and kernel_sha256() == TRAFFIC_KERNEL_SHA256 else None),
+                "ops_per_mapping": ops, "kernel_ms": avg_launch_s * 1e3}
+    if args.mode != "search":
+        roofline = None  # several kernels and host steps per call: no single roofline
     line = {
         "metric": "mappings evaluated/sec (3^N brute force, N=19) + % of VALU peak",
         "value": value,
-        "unit": "mappings/s",
+        "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -199,16 +239,15 @@ def main():
         "dtype": "u32",
         "data": "synthetic",
         "config": {"workload": workloads[args.config], "n_tools": n_tools,
-                   "mappings_per_step": total, "parallelism": "single GPU"},
-        "roofline": {"bound": "alu", "achieved": achieved / 1e12,
-                     "peak": VALU_PEAK_OPS / 1e12, "unit": "Tops/s (int32 VALU lane-ops)",
-                     "frac": achieved / VALU_PEAK_OPS,
-                     "traffic": (TRAFFIC_BYTES if args.config == HEADLINE_CONFIG and
-                                 kernel_sha256() == TRAFFIC_KERNEL_SHA256 else None),
-                     "ops_per_mapping": ops, "kernel_ms": avg_launch_s * 1e3},
+                   "mappings_per_step": total, "parallelism": "single GPU",
+                   "contention": "processor sharing" if args.sharing else "fixed at start",
+                   "mode": args.mode},
+        "roofline": roofline,
         "check": check,
     }
-    if not args.no_cpu_baseline and args.config != 4:
+    line.update(extra)
+    if not args.no_cpu_baseline and args.config != 4 and args.mode == "search" and \
+            not args.sharing:
         line["cpu_baseline"] = cpu_baseline(inst)
     print(json.dumps(line), flush=True)
 

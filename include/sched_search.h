@@ -47,7 +47,8 @@ extern "C" {
 #define SCHED_E_VALUE (-3)     /* gpu_us or cpu_us < 1; load, xfer, mem or
                                   budget < 0; a factor < 65536 or > 2^24; an
                                   option mask outside [1, 7]; a mode that the
-                                  problem does not allow */
+                                  problem does not allow; a contention mode
+                                  other than 0 or 1 */
 #define SCHED_E_EDGE (-4)      /* edge endpoint out of range, or a self-loop */
 #define SCHED_E_CYCLE (-5)     /* the edges contain a cycle */
 #define SCHED_E_RANGE (-6)     /* lo >= hi or hi > the number of mappings; an
@@ -113,6 +114,29 @@ int sched_problem_create_masked(const sched_tool *tools, int32_t n_tools,
                                 const uint32_t *contention_q16, int32_t n_levels,
                                 int64_t vram_budget_mib, const uint8_t *allowed,
                                 sched_problem **out);
+
+/* All creation parameters in one place (the two calls above are shorthands).
+ * allowed: as for sched_problem_create_masked, or null for every mode.
+ * contention_mode: how concurrent GPU tools slow each other (Section 2.3,
+ * Factor A; the paper measures it and states no rule):
+ *   0  fixed at start: a GPU tool starting while k GPU tools run (itself
+ *      included) lasts round(b * F[min(k, K)] / 2^16), for its whole run;
+ *   1  processor sharing: every running GPU tool advances at 1 / F[min(k, K)]
+ *      of its isolated speed, k recounted at every start and end (work in
+ *      units of 2^-16 us, rates round(2^32 / F) halves up). */
+typedef struct {
+    const sched_tool *tools;
+    int32_t n_tools;
+    const sched_edge *edges;
+    int32_t n_edges;
+    const uint32_t *contention_q16;
+    int32_t n_levels;
+    int64_t vram_budget_mib;
+    const uint8_t *allowed;
+    int32_t contention_mode;
+} sched_problem_desc;
+
+int sched_problem_create_desc(const sched_problem_desc *desc, sched_problem **out);
 
 void sched_problem_destroy(sched_problem *p);
 

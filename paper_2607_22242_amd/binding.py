@@ -23,7 +23,8 @@ ERRORS = {
 NO_INDEX = (1 << 64) - 1
 INFEASIBLE = (1 << 63) - 1
 
-EXPORTED = ["sched_problem_create", "sched_problem_create_masked", "sched_problem_destroy",
+EXPORTED = ["sched_problem_create", "sched_problem_create_masked", "sched_problem_create_desc",
+            "sched_problem_destroy",
             "sched_mapping_modes", "sched_mapping_index", "sched_num_tools",
             "sched_num_mappings", "sched_workspace_bytes", "sched_bruteforce_argmin",
             "sched_eval_batch", "sched_eval_mappings", "sched_eval_reprobes",
@@ -55,6 +56,14 @@ class sched_probe(ctypes.Structure):
     _fields_ = [("index", ctypes.c_uint64), ("makespan_us", ctypes.c_int64),
                 ("kind", ctypes.c_int32), ("tool", ctypes.c_int32),
                 ("mode", ctypes.c_int32), ("swap_tool", ctypes.c_int32)]
+
+
+class sched_problem_desc(ctypes.Structure):
+    _fields_ = [("tools", ctypes.c_void_p), ("n_tools", ctypes.c_int32),
+                ("edges", ctypes.c_void_p), ("n_edges", ctypes.c_int32),
+                ("contention_q16", ctypes.c_void_p), ("n_levels", ctypes.c_int32),
+                ("vram_budget_mib", ctypes.c_int64), ("allowed", ctypes.c_void_p),
+                ("contention_mode", ctypes.c_int32)]
 
 
 class sched_prune_stats(ctypes.Structure):
@@ -90,6 +99,9 @@ def lib():
         L.sched_problem_create_masked.argtypes = [P, ctypes.c_int32, P, ctypes.c_int32, P,
                                                   ctypes.c_int32, ctypes.c_int64, P,
                                                   ctypes.POINTER(ctypes.c_void_p)]
+        L.sched_problem_create_desc.restype = ctypes.c_int
+        L.sched_problem_create_desc.argtypes = [ctypes.POINTER(sched_problem_desc),
+                                                ctypes.POINTER(ctypes.c_void_p)]
         L.sched_mapping_modes.restype = ctypes.c_int
         L.sched_mapping_modes.argtypes = [P, ctypes.c_uint64, P]
         L.sched_mapping_index.restype = ctypes.c_int
@@ -173,6 +185,26 @@ def sched_problem_create_masked(tools, edges, contention_q16, vram_budget_mib: i
     rc = lib().sched_problem_create_masked(*_problem_args(tools, edges, contention_q16),
                                            int(vram_budget_mib), a, ctypes.byref(h))
     _check(rc, "sched_problem_create_masked")
+    return h
+
+
+def sched_problem_create_desc(tools, edges, contention_q16, vram_budget_mib: int,
+                              allowed: Optional[Sequence[int]] = None,
+                              contention_mode: int = 0):
+    """The general creation call: optional mode masks, and the contention
+    reading (0 fixed at start, 1 processor sharing)."""
+    t, n, e, ne, f, nl = _problem_args(tools, edges, contention_q16)
+    a = None
+    if allowed is not None:
+        a = (ctypes.c_uint8 * max(len(allowed), 1))(*map(int, allowed))
+    d = sched_problem_desc(ctypes.cast(t, ctypes.c_void_p), n,
+                           ctypes.cast(e, ctypes.c_void_p) if e is not None else None, ne,
+                           ctypes.cast(f, ctypes.c_void_p), nl, int(vram_budget_mib),
+                           ctypes.cast(a, ctypes.c_void_p) if a is not None else None,
+                           int(contention_mode))
+    h = ctypes.c_void_p()
+    _check(lib().sched_problem_create_desc(ctypes.byref(d), ctypes.byref(h)),
+           "sched_problem_create_desc")
     return h
 
 
@@ -372,8 +404,13 @@ class Monitor:
 
 
 class Problem:
-    def __init__(self, tools, edges, contention_q16, vram_budget_mib, allowed=None):
-        if allowed is None:
+    def __init__(self, tools, edges, contention_q16, vram_budget_mib, allowed=None,
+                 sharing: bool = False):
+        self.handle = None
+        if sharing:
+            self.handle = sched_problem_create_desc(tools, edges, contention_q16,
+                                                    vram_budget_mib, allowed, 1)
+        elif allowed is None:
             self.handle = sched_problem_create(tools, edges, contention_q16, vram_budget_mib)
         else:
             self.handle = sched_problem_create_masked(tools, edges, contention_q16,
@@ -382,13 +419,13 @@ class Problem:
         self.n_mappings = sched_num_mappings(self.handle)
 
     @classmethod
-    def from_instance(cls, inst, allowed=None):
+    def from_instance(cls, inst, allowed=None, sharing: bool = False):
         """A problem from an instance dict; its "allowed" mode masks, if any,
         unless `allowed` is given."""
         if allowed is None:
             allowed = inst.get("allowed")
         return cls(inst["tools"], inst["edges"], inst["contention_q16"], inst["vram_budget_mib"],
-                   allowed)
+                   allowed, sharing)
 
     def close(self):
         if self.handle is not None:

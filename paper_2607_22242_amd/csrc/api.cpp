@@ -26,6 +26,7 @@ struct sched_problem {
   std::vector<uint64_t> weight;             // W_v: product of the radices of tools < v
   std::vector<int32_t> enum_tools;          // tools with radix > 1, ascending
   int64_t budget = 0;
+  int32_t sharing = 0;                      // 1: processor-sharing contention
   uint64_t n_mappings = 0;
   int32_t n_preds = 0;
   uint32_t table_words = 0;
@@ -166,15 +167,37 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
   out[kHdrBigLo] = uint32_t(big);
   out[kHdrBigHi] = uint32_t(big >> 32);
   out[kHdrDurOff] = dur_off;
-  // Bound table: shortest durations per mode and over the allowed modes.
+  // Processor-sharing table: isolated GPU latencies per label, then the
+  // work rate of each contention level, round(2^32 / F) halves up.
   const uint32_t bound_off = dur_off + uint32_t(n) * 2u * uint32_t(levels);
+  const uint32_t share_off = bound_off + kBoundWords * uint32_t(n);
+  for (int i = 0; i < n; ++i) {
+    const int v = p.order[i];
+    const int64_t gpu = lat ? lat[v].gpu_us : p.tools[v].gpu_us;
+    const int64_t load = lat ? lat[v].load_us : p.tools[v].load_us;
+    out[share_off + 2 * uint32_t(i)] = uint32_t(gpu);
+    out[share_off + 2 * uint32_t(i) + 1] = uint32_t(gpu + load);
+  }
+  for (int l = 0; l < levels; ++l) {
+    const uint64_t f = p.contention[l];
+    out[share_off + 2 * uint32_t(n) + uint32_t(l)] = uint32_t(((1ull << 33) + f) / (2 * f));
+  }
+  out[kHdrShareOff] = share_off;
+  // Bound table: shortest durations per mode and over the allowed modes.
+  // Fixed at start, a GPU task lasts one of its scaled durations; under
+  // processor sharing at least its work over the fastest rate.
   for (int i = 0; i < n; ++i) {
     const int v = p.order[i];
     uint32_t best[3] = {out[kHdrWords + kToolWords * uint32_t(i) + kToolCpu], kInf, kInf};
     if (!((big >> i) & 1))
       for (int q = 0; q < 2; ++q)
         for (int l = 0; l < levels; ++l) {
-          const uint32_t d = out[dur_off + (uint32_t(i) * 2u + uint32_t(q)) * uint32_t(levels) + l];
+          uint32_t d = out[dur_off + (uint32_t(i) * 2u + uint32_t(q)) * uint32_t(levels) + l];
+          if (p.sharing) {
+            const uint64_t work = uint64_t(out[share_off + 2 * uint32_t(i) + uint32_t(q)]) << 16;
+            const uint64_t w = out[share_off + 2 * uint32_t(n) + uint32_t(l)];
+            d = uint32_t((work + w - 1) / w);
+          }
           best[1 + q] = std::min(best[1 + q], d);
         }
     uint32_t any = kInf;
@@ -212,7 +235,7 @@ std::vector<int32_t> enumeration(const sched_problem& p, bool full, int J) {
 
 // Replicas whose problems share this key share one search plan.
 std::vector<uint8_t> plan_key(const sched_problem& p) {
-  std::vector<uint8_t> k{uint8_t(p.n)};
+  std::vector<uint8_t> k{uint8_t(p.n), uint8_t(p.sharing)};
   for (int32_t v : p.late)
     if (p.radix[v] > 1) k.push_back(p.radix[v]);
   return k;
@@ -251,6 +274,7 @@ void plan_search(const sched_problem& p, uint64_t lo, uint64_t hi, uint32_t n_ta
   a.blocks_per_table = uint32_t(std::min<uint64_t>(a.items_per_table, cap));
   a.n_tables = n_tables;
   a.full_range = full ? 1u : 0u;
+  a.sharing = uint32_t(p.sharing);
 }
 
 // Write the enumeration order seq into a table built by build_table.
@@ -295,7 +319,8 @@ int check_workspace(void* ws, size_t ws_bytes, size_t need) {
 
 int create_problem(const sched_tool* tools, int32_t n_tools, const sched_edge* edges,
                    int32_t n_edges, const uint32_t* contention_q16, int32_t n_levels,
-                   int64_t vram_budget_mib, const uint8_t* allowed, sched_problem** out) {
+                   int64_t vram_budget_mib, const uint8_t* allowed, int32_t sharing,
+                   sched_problem** out) {
   if (out == nullptr || tools == nullptr || contention_q16 == nullptr) return SCHED_E_NULL;
   if (n_edges > 0 && edges == nullptr) return SCHED_E_NULL;
   if (n_tools < 1 || n_tools > kMaxTools || n_edges < 0 || n_levels < 1 || n_levels > kMaxLevels)
@@ -311,11 +336,13 @@ int create_problem(const sched_tool* tools, int32_t n_tools, const sched_edge* e
   if (allowed != nullptr)
     for (int32_t v = 0; v < n_tools; ++v)
       if (allowed[v] < 1 || allowed[v] > 7) return SCHED_E_VALUE;
+  if (sharing != 0 && sharing != 1) return SCHED_E_VALUE;
 
   sched_problem* p = new (std::nothrow) sched_problem;
   if (p == nullptr) return SCHED_E_NOMEM;
   try {
     p->n = n_tools;
+    p->sharing = sharing;
     p->tools.assign(tools, tools + n_tools);
     p->contention.assign(contention_q16, contention_q16 + n_levels);
     p->budget = vram_budget_mib;
@@ -518,7 +545,13 @@ int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_e
                          int32_t n_edges, const uint32_t* contention_q16, int32_t n_levels,
                          int64_t vram_budget_mib, sched_problem** out) {
   return create_problem(tools, n_tools, edges, n_edges, contention_q16, n_levels,
-                        vram_budget_mib, nullptr, out);
+                        vram_budget_mib, nullptr, 0, out);
+}
+
+int sched_problem_create_desc(const sched_problem_desc* d, sched_problem** out) {
+  if (d == nullptr) return SCHED_E_NULL;
+  return create_problem(d->tools, d->n_tools, d->edges, d->n_edges, d->contention_q16,
+                        d->n_levels, d->vram_budget_mib, d->allowed, d->contention_mode, out);
 }
 
 int sched_problem_create_masked(const sched_tool* tools, int32_t n_tools,
@@ -528,7 +561,7 @@ int sched_problem_create_masked(const sched_tool* tools, int32_t n_tools,
                                 sched_problem** out) {
   if (allowed == nullptr) return SCHED_E_NULL;
   return create_problem(tools, n_tools, edges, n_edges, contention_q16, n_levels,
-                        vram_budget_mib, allowed, out);
+                        vram_budget_mib, allowed, 0, out);
 }
 
 void sched_problem_destroy(sched_problem* p) { delete p; }
@@ -740,7 +773,7 @@ int sched_eval_mappings(const sched_problem* p, const uint64_t* d_idx, int64_t n
   HIP_TRY(hipMemcpyAsync(d_workspace, p->table.data(), size_t(p->table_words) * 4,
                          hipMemcpyHostToDevice, s));
   HIP_TRY(launch_eval(p->n, static_cast<const uint32_t*>(d_workspace), d_idx, n, p->n_mappings,
-                      d_makespan, s));
+                      d_makespan, uint32_t(p->sharing), s));
   HIP_TRY(hipStreamSynchronize(s));
   return SCHED_OK;
 }
@@ -790,7 +823,7 @@ int sched_eval_reprobes(const sched_problem* p, uint64_t base_index, const sched
                          hipMemcpyHostToDevice, s));
   HIP_TRY(hipMemcpyAsync(d_idx, idx.data(), m * 8, hipMemcpyHostToDevice, s));
   HIP_TRY(launch_eval(n, reinterpret_cast<const uint32_t*>(ws + L.tables), d_idx, int64_t(m),
-                      p->n_mappings, d_ms, s));
+                      p->n_mappings, d_ms, uint32_t(p->sharing), s));
   HIP_TRY(hipMemcpyAsync(ms.data(), d_ms, m * 8, hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   // Keep a swap only when its move to gpu_now was infeasible.
@@ -865,7 +898,8 @@ int sched_pruned_argmin(const sched_problem* p, void* d_workspace, size_t ws_byt
         uint64_t* d_idx = reinterpret_cast<uint64_t*>(ws + L.probe_idx);
         int64_t* d_ms = reinterpret_cast<int64_t*>(ws + L.probe_ms);
         HIP_TRY(hipMemcpyAsync(d_idx, idx.data(), idx.size() * 8, hipMemcpyHostToDevice, s));
-        HIP_TRY(launch_eval(n, d_tab, d_idx, int64_t(idx.size()), p->n_mappings, d_ms, s));
+        HIP_TRY(launch_eval(n, d_tab, d_idx, int64_t(idx.size()), p->n_mappings, d_ms,
+                            uint32_t(p->sharing), s));
         HIP_TRY(hipMemcpyAsync(ms.data(), d_ms, idx.size() * 8, hipMemcpyDeviceToHost, s));
         HIP_TRY(hipStreamSynchronize(s));
         ++st.descent_rounds;

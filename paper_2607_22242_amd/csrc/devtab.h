@@ -39,6 +39,7 @@ enum : uint32_t {
   kHdrBaseLo = 11,    // index contribution of the fixed tools (a subspace's
   kHdrBaseHi = 12,    // offset in the mapping index)
   kHdrBoundOff = 13,  // word offset of the bound table
+  kHdrShareOff = 14,  // word offset of the processor-sharing table
   kHdrWords = 16,
 };
 
@@ -83,9 +84,14 @@ inline constexpr uint32_t opt_mode(uint32_t o, uint32_t d) { return (o >> (2u + 
 // tool whose footprint exceeds the budget (it can never run there).
 constexpr uint32_t kBoundWords = 4;
 
+// Processor-sharing table (after the bound table): for internal label i,
+// b[2i] = gpu_us and b[2i + 1] = gpu_us + load_us (isolated latencies), then
+// for each contention level the work rate round(2^32 / F) in 2^-16 us of
+// isolated work per us.
 inline uint32_t table_words(int n, int n_preds, int levels) {
   uint32_t dur_off = kPredBase + ((uint32_t(n_preds) + 3u) & ~3u);
-  return dur_off + uint32_t(n) * 2u * uint32_t(levels) + kBoundWords * uint32_t(n);
+  return dur_off + uint32_t(n) * 2u * uint32_t(levels) + kBoundWords * uint32_t(n) +
+         2u * uint32_t(n) + uint32_t(levels);
 }
 
 struct Partial {
@@ -107,6 +113,7 @@ struct SearchArgs {
   uint64_t items_per_table;   // ceil(n_outer / kBlock)
   uint32_t blocks_per_table;
   uint32_t full_range;        // 1: [lo, hi) is every mapping, any enumeration order
+  uint32_t sharing;           // 1: processor-sharing contention
 };
 
 struct DevResult {

@@ -15,7 +15,7 @@ template <int N>
 hipError_t launch_search_n(const SearchArgs& a, hipStream_t s);
 template <int N>
 hipError_t launch_eval_n(const uint32_t* tab, const uint64_t* idx, int64_t n, uint64_t n_mappings,
-                         int64_t* out, hipStream_t s);
+                         int64_t* out, uint32_t sharing, hipStream_t s);
 template <int N>
 hipError_t launch_bound_n(const uint32_t* tab, uint32_t K, uint64_t known, int64_t n,
                           uint32_t* out, hipStream_t s);
@@ -67,7 +67,7 @@ __global__ __launch_bounds__(kBlock) void reduce_kernel(const Partial* __restric
 
 using SearchFn = hipError_t (*)(const SearchArgs&, hipStream_t);
 using EvalFn = hipError_t (*)(const uint32_t*, const uint64_t*, int64_t, uint64_t, int64_t*,
-                              hipStream_t);
+                              uint32_t, hipStream_t);
 
 template <size_t... I>
 static constexpr auto make_search_table(std::index_sequence<I...>) {
@@ -93,8 +93,8 @@ hipError_t launch_search(int n_tools, const SearchArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_eval(int n_tools, const uint32_t* tab, const uint64_t* idx, int64_t n,
-                       uint64_t n_mappings, int64_t* out, hipStream_t s) {
-  return kEvalFns[n_tools - 1](tab, idx, n, n_mappings, out, s);
+                       uint64_t n_mappings, int64_t* out, uint32_t sharing, hipStream_t s) {
+  return kEvalFns[n_tools - 1](tab, idx, n, n_mappings, out, sharing, s);
 }
 
 hipError_t launch_bound(int n_tools, const uint32_t* tab, uint32_t K, uint64_t known, int64_t n,

@@ -12,7 +12,7 @@ namespace devmap {
 #define DEVMAP_INST(N)                                                            \
   template hipError_t launch_search_n<N>(const SearchArgs&, hipStream_t);         \
   template hipError_t launch_eval_n<N>(const uint32_t*, const uint64_t*, int64_t, \
-                                       uint64_t, int64_t*, hipStream_t);          \
+                                       uint64_t, int64_t*, uint32_t, hipStream_t); \
   template hipError_t launch_bound_n<N>(const uint32_t*, uint32_t, uint64_t, int64_t, \
                                         uint32_t*, hipStream_t);
 

@@ -365,6 +365,133 @@ __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict
   return ms;
 }
 
+// Makespan under processor sharing, or kInf if infeasible.  The events are
+// those of the fixed-at-start schedule (release, immediate starts with the
+// VRAM check, one queue admission in (ready, tool) order), but a GPU task's
+// end is not fixed when it starts: every running GPU task advances at the
+// rate w_k of the k GPU tasks running, so with V the work each has done
+// since time 0, a task started at V_s with work b * 2^16 ends when V reaches
+// its virtual finish V_s + b * 2^16.  Per lane: X[i] holds the ready time of
+// a waiting task and the end of a started one.
+template <int N>
+__host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __restrict__ tab,
+                                                              const uint32_t* __restrict__ lds,
+                                                              uint32_t levels, uint32_t budget,
+                                                              MaskT<N> gnm, MaskT<N> gqm) {
+  using M = MaskT<N>;
+  const Tab tp{tab};
+  const uint32_t* s_mem = lds + lds_mem_off<N>();
+  const uint32_t* sh = tab + tab[kHdrShareOff];
+  const M gpu = gnm | gqm;
+  if ((gpu & load_mask<N>(tp, kHdrBigLo)) != 0) return kInf;
+  uint32_t X[N];
+  uint64_t VF[N];
+  M running = 0, done = 0;
+  uint64_t V = 0;
+  uint32_t t = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    X[i] = 0;
+    VF[i] = 0;
+  }
+  for (int pass = 0; pass < 4 * N + 4; ++pass) {
+    // 1. release: CPU tasks at their end, GPU tasks out of work
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if ((running >> i) & 1) {
+        const bool fin = ((gpu >> i) & 1) ? VF[i] <= V : X[i] <= t;
+        if (fin) {
+          running &= ~(M(1) << i);
+          done |= M(1) << i;
+          X[i] = t;
+        }
+      }
+    }
+    if (done == all_tools<N>()) return t;
+    // 2. ready times of waiting tasks whose predecessors are done, and the
+    // immediate starts
+    const M waiting = ~(running | done) & all_tools<N>();
+    M ready = 0, starting = 0;
+    uint32_t in_use = 0;
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if ((running >> i) & 1 && (gpu >> i) & 1) in_use += s_mem[i];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if ((waiting >> i) & 1) {
+        const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
+        if ((pm & ~done) == 0) {
+          const uint32_t xf = tp[kHdrWords + kToolWords * i + kToolXfer];
+          uint32_t r = 0;
+#pragma unroll
+          for (int u = 0; u < i; ++u)
+            if ((pm >> u) & 1)
+              r = umax32(r, X[u] + ((((gpu >> u) ^ (gpu >> i)) & 1) ? xf : 0u));
+          X[i] = r;
+          ready |= M(1) << i;
+          if (r <= t && !((gqm >> i) & 1)) {
+            starting |= M(1) << i;
+            if ((gnm >> i) & 1) in_use += s_mem[i];
+          }
+        }
+      }
+    }
+    if (in_use > budget) return kInf;
+    // 3. one queue admission when no queued task runs: FIFO on (ready, tool)
+    if ((running & gqm) == 0) {
+      int head = -1;
+      uint32_t hr = kInf, ho = kInf;
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        if ((ready >> i) & 1 && (gqm >> i) & 1 && X[i] <= t) {
+          const uint32_t o = tp[kHdrWords + kToolWords * i + kToolOrig];
+          if (X[i] < hr || (X[i] == hr && o < ho)) {
+            head = i;
+            hr = X[i];
+            ho = o;
+          }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < N; ++i)
+        if (i == head && s_mem[i] <= budget - in_use) starting |= M(1) << i;
+    }
+    // 4. starts
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if ((starting >> i) & 1) {
+        if ((gpu >> i) & 1)
+          VF[i] = V + (uint64_t(sh[2 * i + (((gqm >> i) & 1) ? 1 : 0)]) << 16);
+        else
+          X[i] = t + tp[kHdrWords + kToolWords * i + kToolCpu];
+      }
+    }
+    running |= starting;
+    // 5. next event at the rate of the GPU tasks now running
+    const M rg = running & gpu;
+    uint32_t next = kInf, k = 0;
+    uint64_t vmin = ~0ull;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if ((rg >> i) & 1) {
+        ++k;
+        vmin = vmin < VF[i] ? vmin : VF[i];
+      }
+      if ((running >> i) & 1 && !((gpu >> i) & 1)) next = umin32(next, X[i]);
+      if ((ready >> i) & 1 && !((starting >> i) & 1) && X[i] > t) next = umin32(next, X[i]);
+    }
+    uint64_t w = 0;
+    if (k) {
+      w = sh[2 * N + (k < levels ? k : levels) - 1];
+      next = umin32(next, t + uint32_t((vmin - V + w - 1) / w));
+    }
+    if (next == kInf) return kInf;  // a queued task never fits
+    V += uint64_t(next - t) * w;
+    t = next;
+  }
+  return kInf;  // not reached: every pass starts, ends or readies a task
+}
+
 __device__ __forceinline__ void lex_min(uint32_t& ms, uint64_t& x, uint32_t oms, uint64_t ox) {
   if (oms < ms || (oms == ms && ox < x)) {
     ms = oms;
@@ -436,6 +563,11 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
 #ifndef DEVMAP_SEARCH_WAVES
 #define DEVMAP_SEARCH_WAVES 8
 #endif
+// The same for the processor-sharing evaluator, which keeps a 64-bit virtual
+// finish per tool.
+#ifndef DEVMAP_SHARE_WAVES
+#define DEVMAP_SHARE_WAVES 2
+#endif
 
 // Index arithmetic: 3^20 < 2^32, so up to 20 tools an index fits 32 bits.
 template <int N>
@@ -450,7 +582,7 @@ using IdxT = typename std::conditional<(N <= 20), uint32_t, uint64_t>::type;
 // index need not grow along the walk, so the running minimum compares
 // (makespan, index) in full.  Otherwise: index order, o * 3^J + i, clipped to
 // [lo, hi); indices grow, so a strict comparison keeps the lowest index.
-template <int N, bool FULL>
+template <int N, bool FULL, bool SHARE>
 __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
                                                      const uint32_t* __restrict__ tab,
                                                      const uint32_t* __restrict__ lds,
@@ -492,7 +624,11 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
   }
   for (uint32_t i = 0; i < a.inner_count; ++i) {
     if (FULL || (i >= ilo && i < ihi)) {
-      const uint32_t ms = evaluate<N>(tab, lds, levels, budget, ogn | ign, ogq | igq, slot);
+      uint32_t ms;
+      if constexpr (SHARE)
+        ms = evaluate_sharing<N>(tab, lds, levels, budget, ogn | ign, ogq | igq);
+      else
+        ms = evaluate<N>(tab, lds, levels, budget, ogn | ign, ogq | igq, slot);
       if constexpr (FULL) {
         if (ms <= best_ms) {
           const I x = xo + xi;
@@ -539,8 +675,8 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // work items (kBlock consecutive outer combinations each) with a stride of
 // blocks_per_table.  Each lane keeps its own (makespan, index) minimum; the
 // block's minimum goes to partials[b].
-template <int N, bool FULL>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(DEVMAP_SEARCH_WAVES))) void search_kernel(SearchArgs a) {
+template <int N, bool FULL, bool SHARE>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(SHARE ? DEVMAP_SHARE_WAVES : DEVMAP_SEARCH_WAVES))) void search_kernel(SearchArgs a) {
   __shared__ uint32_t s_lds[lds_words<N>()];
   __shared__ MaskT<N> s_wave[kBlock / 64];
   const uint32_t table = blockIdx.x / a.blocks_per_table;
@@ -551,8 +687,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(DEVMAP_S
   uint32_t best_ms = kInf;
   uint64_t best_x = ~0ull;
   for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-    lane_search<N, FULL>(a, tab, s_lds, item, threadIdx.x, &s_wave[threadIdx.x / 64], best_ms,
-                         best_x);
+    lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x, &s_wave[threadIdx.x / 64],
+                                best_ms, best_x);
 
   block_min(best_ms, best_x);
   if (threadIdx.x == 0) {
@@ -565,7 +701,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(DEVMAP_S
 }
 
 // Score explicit indices (grid-stride).
-template <int N>
+template <int N, bool SHARE>
 __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict__ tab,
                                                       const uint64_t* __restrict__ idx,
                                                       int64_t n, uint64_t n_mappings,
@@ -584,7 +720,11 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
       M gn, gq;
       uint64_t xw;
       decode_positions<N>(tab, x, 0, tab[kHdrPositions], gn, gq, xw);
-      const uint32_t ms = evaluate<N>(tab, s_lds, levels, budget, gn, gq, &s_wave[threadIdx.x / 64]);
+      uint32_t ms;
+      if constexpr (SHARE)
+        ms = evaluate_sharing<N>(tab, s_lds, levels, budget, gn, gq);
+      else
+        ms = evaluate<N>(tab, s_lds, levels, budget, gn, gq, &s_wave[threadIdx.x / 64]);
       if (ms != kInf) r = int64_t(ms);
     }
     out[i] = r;
@@ -652,10 +792,17 @@ __global__ __launch_bounds__(kBlock) void bound_kernel(const uint32_t* __restric
 template <int N>
 hipError_t launch_search_n(const SearchArgs& a, hipStream_t s) {
   const uint32_t blocks = a.n_tables * a.blocks_per_table;
-  if (a.full_range)
-    hipLaunchKernelGGL((search_kernel<N, true>), dim3(blocks), dim3(kBlock), 0, s, a);
-  else
-    hipLaunchKernelGGL((search_kernel<N, false>), dim3(blocks), dim3(kBlock), 0, s, a);
+  if (a.sharing) {
+    if (a.full_range)
+      hipLaunchKernelGGL((search_kernel<N, true, true>), dim3(blocks), dim3(kBlock), 0, s, a);
+    else
+      hipLaunchKernelGGL((search_kernel<N, false, true>), dim3(blocks), dim3(kBlock), 0, s, a);
+  } else {
+    if (a.full_range)
+      hipLaunchKernelGGL((search_kernel<N, true, false>), dim3(blocks), dim3(kBlock), 0, s, a);
+    else
+      hipLaunchKernelGGL((search_kernel<N, false, false>), dim3(blocks), dim3(kBlock), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -672,12 +819,17 @@ hipError_t launch_bound_n(const uint32_t* tab, uint32_t K, uint64_t known, int64
 
 template <int N>
 hipError_t launch_eval_n(const uint32_t* tab, const uint64_t* idx, int64_t n,
-                                uint64_t n_mappings, int64_t* out, hipStream_t s) {
+                                uint64_t n_mappings, int64_t* out, uint32_t sharing,
+                                hipStream_t s) {
   int64_t blocks = (n + kBlock - 1) / kBlock;
   if (blocks > 65536) blocks = 65536;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(eval_kernel<N>, dim3(uint32_t(blocks)), dim3(kBlock), 0, s, tab, idx, n,
-                     n_mappings, out);
+  if (sharing)
+    hipLaunchKernelGGL((eval_kernel<N, true>), dim3(uint32_t(blocks)), dim3(kBlock), 0, s, tab,
+                       idx, n, n_mappings, out);
+  else
+    hipLaunchKernelGGL((eval_kernel<N, false>), dim3(uint32_t(blocks)), dim3(kBlock), 0, s, tab,
+                       idx, n, n_mappings, out);
   return hipGetLastError();
 }
 

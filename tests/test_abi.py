@@ -165,6 +165,16 @@ def test_pruned_search_validation():
     assert S.sched_pruned_workspace_bytes(small.handle) == S.sched_workspace_bytes([small.handle])
 
 
+def test_problem_desc_validation():
+    c = S.sched_problem_create_desc
+    assert err(c, [TOOL] * 2, [], F, 100, None, 2) == "SCHED_E_VALUE"
+    assert err(c, [TOOL] * 2, [], F, 100, [3, 9], 1) == "SCHED_E_VALUE"
+    h = ctypes.c_void_p()
+    assert B.ERRORS[B.lib().sched_problem_create_desc(None, ctypes.byref(h))] == "SCHED_E_NULL"
+    P = S.Problem([TOOL] * 3, [[0, 1]], F, 100, [3, 7, 1], sharing=True)
+    assert P.n_mappings == 6
+
+
 def test_strerror_covers_codes():
     for code, name in B.ERRORS.items():
         assert S.sched_strerror(code) != "unknown error", name

@@ -539,3 +539,82 @@ def test_pruned_search_beyond_the_oracle(torch_cuda, O):
     assert st["initial_bound_us"] >= bm
     say("exhaustive n=22")
     assert gpu_argmin(torch_cuda, P) == (bi, bm)
+
+
+# ---------------------------------------------------------------------------
+# Processor-sharing contention.
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_sharing_every_index_and_search(torch_cuda, O, seed):
+    n = 1 + seed % 8
+    inst = synth.random_instance(5500 + seed, n, ["random", "permuted", "fanout", "chain"][seed % 4],
+                                 tight=seed % 2 == 0, small_values=seed % 3 == 0)
+    P = S.Problem.from_instance(inst, sharing=True)
+    Q = O.Problem.from_instance(inst, sharing=True)
+    idx = np.arange(P.n_mappings, dtype=np.uint64)
+    say(f"sharing seed {seed} n={n}")
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, idx), Q.eval_many(idx))
+    assert gpu_argmin(torch_cuda, P) == Q.argmin()
+    b = P.n_mappings // 2
+    assert S.sched_eval_reprobes(P.handle, b, S.workspace([P.handle])) == O.reprobes(Q, b)
+
+
+def test_sharing_configs(torch_cuda, O):
+    inst = synth.load(1)
+    P = S.Problem.from_instance(inst, sharing=True)
+    Q = O.Problem.from_instance(inst, sharing=True)
+    say("sharing config 1 full")
+    assert gpu_argmin(torch_cuda, P) == Q.argmin()
+    inst = synth.load(2)
+    P = S.Problem.from_instance(inst, sharing=True)
+    Q = O.Problem.from_instance(inst, sharing=True)
+    rng = np.random.default_rng(12)
+    idx = rng.integers(0, P.n_mappings, 50000, dtype=np.uint64)
+    say("sharing config 2 sampled")
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, idx), Q.eval_many(idx))
+    say("sharing config 2 pruned vs exhaustive")
+    bi, bm, st = pruned(P)
+    assert gpu_argmin(torch_cuda, P) == (bi, bm)
+    assert Q.eval_index(bi) == bm
+    inst = synth.load(3)
+    P = S.Problem.from_instance(inst, sharing=True)
+    Q = O.Problem.from_instance(inst, sharing=True)
+    idx = rng.integers(0, P.n_mappings, 20000, dtype=np.uint64)
+    say("sharing config 3 sampled")
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, idx), Q.eval_many(idx))
+
+
+def test_sharing_paper_scenarios(torch_cuda, O):
+    d = json.load(open(os.path.join(GOLDEN, "paper_scenarios.json")))
+    for name in ["S1", "S5", "S13"]:
+        s = d["scenarios"][name]
+        edges = d["diamond_edges"] if s["topology"] == "diamond" else []
+        allowed = [3, 3, 3, 3] if name != "S13" else None
+        P = S.Problem(s["tools"], edges, d["contention_q16"], s["budget"], allowed, sharing=True)
+        Q = O.Problem(s["tools"], edges, d["contention_q16"], s["budget"], sharing=True)
+        want = O.masked_argmin(Q, O.Space(allowed or [7] * 4))
+        assert gpu_argmin(torch_cuda, P) == want, name
+        if name == "S1":
+            assert S.sched_mapping_modes(P.handle, want[0]) == s["paper_oracle"]
+
+
+def test_sharing_batch_and_wide(torch_cuda, O):
+    """A batch mixing both readings; a 40-tool problem under sharing."""
+    insts = [synth.random_instance(5600 + s, 6, "random", tight=True) for s in range(2)]
+    probs = [S.Problem.from_instance(insts[0]), S.Problem.from_instance(insts[0], sharing=True),
+             S.Problem.from_instance(insts[1], sharing=True)]
+    rp = [0, 1, 2, 1, 0]
+    src = [0, 0, 1]
+    lats = [[[t[0] + 11 * r, t[1] + 5 * r, t[2], t[3]] for t in insts[src[pi]]["tools"]]
+            for r, pi in enumerate(rp)]
+    handles = [p.handle for p in probs]
+    got = S.sched_eval_batch(handles, rp, lats, S.workspace(handles, len(rp)))
+    for r, pi in enumerate(rp):
+        Q = O.Problem.from_instance(insts[src[pi]], lats[r], sharing=pi > 0)
+        assert tuple(got[r]) == Q.argmin(), r
+    inst = synth.random_instance(5700, 40, "permuted", tight=True)
+    P = S.Problem.from_instance(inst, sharing=True)
+    Q = O.Problem.from_instance(inst, sharing=True)
+    idx = np.random.default_rng(3).integers(0, P.n_mappings, 5000, dtype=np.uint64)
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, idx), Q.eval_many(idx))
