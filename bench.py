@@ -14,7 +14,9 @@ single search of a 32-tool DAG in the GPU/CPU space (2^30 mappings).
 --sharing scores mappings under processor-sharing contention instead of the
 fixed-at-start reading.  --mode pruned times the exact pruned search (value:
 mappings of the whole space per second); --mode reprobes times one what-if
-exploration around the optimum (value: probes per second).
+exploration around the optimum (value: probes per second).  --random-tools N
+--random-seed S [--tight] replaces the config by a random DAG of
+workloads.synth.random_instance (for the pruned search beyond 3^19).
 """
 from __future__ import annotations
 
@@ -98,6 +100,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--config", type=int, default=HEADLINE_CONFIG, choices=range(6))
     ap.add_argument("--sharing", action="store_true")
+    ap.add_argument("--random-tools", type=int, default=0)
+    ap.add_argument("--random-seed", type=int, default=9990)
+    ap.add_argument("--tight", action="store_true")
     ap.add_argument("--mode", default="search", choices=["search", "pruned", "reprobes"])
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only run one plain device-to-device copy of this many MiB "
@@ -123,7 +128,11 @@ def main():
     import paper_2607_22242_amd as S
     from workloads import synth
 
-    inst = synth.load(args.config)
+    if args.random_tools:
+        inst = synth.random_instance(args.random_seed, args.random_tools, "random",
+                                     tight=args.tight)
+    else:
+        inst = synth.load(args.config)
     stream = torch.cuda.current_stream()
     extra = {}
     if args.mode != "search":
@@ -182,7 +191,7 @@ def main():
 
     exp_path = os.path.join(ROOT, "tests", "golden", "expected_configs.json")
     expected = None
-    if os.path.exists(exp_path) and not args.sharing:
+    if os.path.exists(exp_path) and not args.sharing and not args.random_tools:
         with open(exp_path) as f:
             expected = json.load(f).get(f"config{args.config}")
     if args.mode == "pruned":
@@ -225,6 +234,11 @@ def main():
                 "ops_per_mapping": ops, "kernel_ms": avg_launch_s * 1e3}
     if args.mode != "search":
         roofline = None  # several kernels and host steps per call: no single roofline
+    if args.random_tools:
+        workloads[args.config] = (f"random{args.random_tools}: random DAG "
+                                  f"({len(inst['edges'])} edges), seed {args.random_seed}"
+                                  f"{', budget a quarter of the footprints' if args.tight else ''}")
+        check.pop("matches_oracle", None)
     line = {
         "metric": "mappings evaluated/sec (3^N brute force, N=19) + % of VALU peak",
         "value": value,
