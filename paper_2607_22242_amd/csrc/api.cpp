@@ -219,11 +219,30 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
 // in tools that act late in every schedule and step through their passes
 // together; the other tools follow from deepest to shallowest.  Any order
 // visits every mapping once.
-std::vector<int32_t> enumeration(const sched_problem& p, bool full, int J) {
+// Full-range searches of problems the shared-prefix kernel serves use
+// kSharedInner inner digits on the deepest tools (the kernel then computes
+// each lane's schedule prefix once for all of their modes) and the next four
+// deepest on the lanes: the plain deepest-first order.
+bool prefix_plan(const sched_problem& p, uint64_t n_tables) {
+  if (p.n > kPrefixMaxN || p.sharing || p.enum_tools.size() < kSharedInner) return false;
+  // enough lanes left to fill the GPU with kSharedInner inner digits
+  const std::vector<int32_t>& v = p.late;
+  uint64_t inner = 1;
+  int taken = 0;
+  for (int32_t t : v)
+    if (p.radix[t] > 1 && taken < int(kSharedInner)) {
+      inner *= p.radix[t];
+      ++taken;
+    }
+  return (unsigned __int128)(p.n_mappings / inner) * n_tables >= kTargetLanes;
+}
+
+std::vector<int32_t> enumeration(const sched_problem& p, bool full, int J, bool prefix) {
   if (!full) return p.enum_tools;
   std::vector<int32_t> late;
   for (int32_t v : p.late)
     if (p.radix[v] > 1) late.push_back(v);
+  if (prefix) return late;
   const int P = int(late.size());
   const int lanes = std::min(4, P - J);
   std::vector<int32_t> seq;
@@ -256,12 +275,17 @@ void plan_search(const sched_problem& p, uint64_t lo, uint64_t hi, uint32_t n_ta
   const int P = int(p.enum_tools.size());
   const unsigned __int128 work = (unsigned __int128)(hi - lo) * n_tables;
   int J = 0;
-  while (J < kMaxInnerDigits && J < P) {
-    const uint64_t next = inner_count(p, enumeration(p, full, J + 1), J + 1);
-    if ((unsigned __int128)next * kTargetLanes > work) break;
-    ++J;
+  const bool prefix = full && prefix_plan(p, n_tables);
+  if (prefix) {
+    J = int(kSharedInner);
+  } else {
+    while (J < kMaxInnerDigits && J < P) {
+      const uint64_t next = inner_count(p, enumeration(p, full, J + 1, false), J + 1);
+      if ((unsigned __int128)next * kTargetLanes > work) break;
+      ++J;
+    }
   }
-  const uint64_t inner = inner_count(p, enumeration(p, full, J), J);
+  const uint64_t inner = inner_count(p, enumeration(p, full, J, prefix), J);
   a.lo = lo;
   a.hi = hi;
   a.inner_digits = uint32_t(J);
@@ -275,6 +299,7 @@ void plan_search(const sched_problem& p, uint64_t lo, uint64_t hi, uint32_t n_ta
   a.n_tables = n_tables;
   a.full_range = full ? 1u : 0u;
   a.sharing = uint32_t(p.sharing);
+  a.prefix = prefix ? 1u : 0u;
 }
 
 // Write the enumeration order seq into a table built by build_table.
@@ -644,7 +669,7 @@ int sched_bruteforce_argmin(const sched_problem* p, uint64_t lo, uint64_t hi, vo
     return SCHED_E_NOMEM;
   }
   if (a.full_range)
-    set_enumeration(*p, enumeration(*p, true, int(a.inner_digits)), table.data());
+    set_enumeration(*p, enumeration(*p, true, int(a.inner_digits), a.prefix != 0), table.data());
   HIP_TRY(hipMemcpyAsync(ws + L.tables, table.data(), size_t(p->table_words) * 4,
                          hipMemcpyHostToDevice, s));
   HIP_TRY(launch_search(p->n, a, s));
@@ -727,7 +752,7 @@ int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
       uint32_t* tb = host_tables.data() + i * max_stride;
       rc = build_table(p, replica_lat + lat_off[r], tb);
       if (rc != SCHED_OK) return rc;
-      set_enumeration(p, enumeration(p, true, int(g.a.inner_digits)), tb);
+      set_enumeration(p, enumeration(p, true, int(g.a.inner_digits), g.a.prefix != 0), tb);
     }
   }
 
@@ -977,7 +1002,7 @@ int sched_pruned_argmin(const sched_problem* p, void* d_workspace, size_t ws_byt
       const uint32_t count = uint32_t(end - next);
       SearchArgs a{};
       plan_search(sub, 0, sub.n_mappings, count, a);
-      set_enumeration(sub, enumeration(sub, true, int(a.inner_digits)), stab.data());
+      set_enumeration(sub, enumeration(sub, true, int(a.inner_digits), a.prefix != 0), stab.data());
       tables.assign(size_t(count) * stride, 0u);
       for (uint32_t t = 0; t < count; ++t) {
         uint32_t* tb = tables.data() + size_t(t) * stride;

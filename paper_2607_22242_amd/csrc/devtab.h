@@ -22,6 +22,8 @@ constexpr int kMaxLevels = 64;
 constexpr uint32_t kInf = 0xFFFFFFFFu;  // "never": unknown ready time, infeasible
 constexpr int kBlock = 256;             // threads per search block (4 waves)
 constexpr int kMaxInnerDigits = 6;      // inner (wave-uniform) digits per lane
+constexpr uint32_t kSharedInner = 3;    // inner digits of a shared-prefix search
+constexpr int kPrefixMaxN = 24;         // tool counts served by shared prefixes
 
 // Header words.
 enum : uint32_t {
@@ -114,6 +116,8 @@ struct SearchArgs {
   uint32_t blocks_per_table;
   uint32_t full_range;        // 1: [lo, hi) is every mapping, any enumeration order
   uint32_t sharing;           // 1: processor-sharing contention
+  uint32_t prefix;            // 1: shared prefixes (kSharedInner inner digits on the
+                              //    deepest tools, full range, fixed at start)
 };
 
 struct DevResult {

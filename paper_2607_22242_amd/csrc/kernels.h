@@ -671,6 +671,166 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
   }
 }
 
+// Shared schedule prefixes.  In a full-range search the inner (wave-uniform)
+// digits are the kSharedInner tools deepest in the DAG.  Until one of them
+// gets a ready time, none of them is waiting, running or resolved, so the
+// schedule of the other tools, and every event time, is the same for all
+// their modes: each lane runs that prefix once per outer combination, keeps
+// the state it had before the first pass that resolves an inner tool, and
+// restarts every inner combination from there.  The state goes to LDS (one
+// column per lane), so it costs no registers.  Tools up to kPrefixMaxN.
+// Every tool's word is saved and restored, inner tools included (they are
+// 0): a branch per tool on the wave-uniform inner mask would be compiled as a
+// lane-mask test that the compiler computes inside the prefix loop and
+// reuses after it, where other lanes are active.
+template <int N>
+constexpr uint32_t snap_words() {
+  // T of every tool, three masks, t, qfin, minq
+  return N <= kPrefixMaxN ? uint32_t(N) + 3u * (N > 32 ? 2u : 1u) + 3u : 1u;
+}
+
+template <int N>
+__host__ __device__ __forceinline__ void snap_mask(uint32_t* s, uint32_t& k, MaskT<N> m) {
+  s[(k++) * kBlock] = uint32_t(m);
+  if constexpr (N > 32) s[(k++) * kBlock] = uint32_t(uint64_t(m) >> 32);
+}
+
+template <int N>
+__host__ __device__ __forceinline__ MaskT<N> unsnap_mask(const uint32_t* s, uint32_t& k) {
+  if constexpr (N > 32) {
+    const uint64_t lo = s[(k++) * kBlock];
+    return lo | (uint64_t(s[(k++) * kBlock]) << 32);
+  } else {
+    return s[(k++) * kBlock];
+  }
+}
+
+// Save / restore a lane's schedule state.  s: this lane's column.
+template <int N>
+__host__ __device__ __forceinline__ void snap_save(uint32_t* s, const Sim<N>& sim) {
+  uint32_t k = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) s[(k++) * kBlock] = sim.T[i];
+  snap_mask<N>(s, k, sim.started);
+  snap_mask<N>(s, k, sim.resolved);
+  snap_mask<N>(s, k, sim.done);
+  s[(k++) * kBlock] = sim.t;
+  s[(k++) * kBlock] = sim.qfin;
+  s[(k++) * kBlock] = sim.minq;
+}
+
+template <int N>
+__host__ __device__ __forceinline__ void snap_load(const uint32_t* s, Sim<N>& sim) {
+  uint32_t k = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) sim.T[i] = s[(k++) * kBlock];
+  sim.started = unsnap_mask<N>(s, k);
+  sim.resolved = unsnap_mask<N>(s, k);
+  sim.done = unsnap_mask<N>(s, k);
+  sim.t = s[(k++) * kBlock];
+  sim.qfin = s[(k++) * kBlock];
+  sim.minq = s[(k++) * kBlock];
+}
+
+// lane_search for a full range with shared prefixes (see above); the inner
+// positions 0..kSharedInner-1 hold the deepest tools.
+template <int N>
+__host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
+                                                            const uint32_t* __restrict__ tab,
+                                                            const uint32_t* __restrict__ lds,
+                                                            uint64_t item, uint32_t lane,
+                                                            MaskT<N>* slot, uint32_t* snap,
+                                                            uint32_t& best_ms, uint64_t& best_x) {
+  using M = MaskT<N>;
+  using I = IdxT<N>;
+  const uint64_t rel = item * kBlock + lane;
+  if (rel >= a.n_outer) return;
+  const uint32_t levels = tab[kHdrLevels];
+  const uint32_t budget = tab[kHdrBudget];
+  constexpr uint32_t J = kSharedInner;
+  M ogn, ogq;
+  uint64_t xo64;
+  decode_positions<N>(tab, a.outer_lo + rel, J, tab[kHdrPositions], ogn, ogq, xo64);
+  // The inner tools (a wave-uniform mask, read through scalar loads).
+  const Tab tu{tab};
+  M inner = 0;
+#pragma unroll
+  for (uint32_t j = 0; j < J; ++j) inner |= M(1) << tu[kEnumLabBase + j];
+  const M big = load_mask<N>(tu, kHdrBigLo);
+
+  // The prefix: inner tools on the CPU (their modes are never read before
+  // one of them is resolved).  pstar: the first pass that resolves one.
+  int pstar = -1;
+  {
+    Sim<N> sim;
+    sim.init(tab, ogn, ogq);
+    for (int pass = 0; pass < 2 * N + 2; ++pass) {
+      snap_save<N>(snap, sim);
+      uint32_t ms;
+      const bool fin = sim.step(tab, lds, levels, budget, pass, slot, ms);
+      if (sim.resolved & inner) {
+        pstar = pass;
+        break;
+      }
+      if (fin) break;  // out of memory or stuck before any inner tool: infeasible
+    }
+  }
+  if (pstar < 0) return;  // every inner combination is infeasible
+
+  I bx = I(best_x);
+  const I xo = I(xo64);
+  M ign = 0, igq = 0;
+  uint32_t idig = 0;
+  I xi = 0;
+#pragma unroll
+  for (uint32_t j = 0; j < J; ++j) {
+    const uint32_t m = opt_mode(tab[kEnumOptBase + j], 0u);
+    const M b = M(1) << tab[kEnumLabBase + j];
+    if (m == 1u) ign |= b;
+    if (m == 2u) igq |= b;
+  }
+  for (uint32_t i = 0; i < a.inner_count; ++i) {
+    Sim<N> sim;
+    snap_load<N>(snap, sim);
+    sim.gnm = ogn | ign;
+    sim.gqm = ogq | igq;
+    sim.dead = ((sim.gnm | sim.gqm) & big) != 0;
+    uint32_t ms = kInf;
+    for (int pass = pstar; pass < 2 * N + 2; ++pass)
+      if (sim.step(tab, lds, levels, budget, pass, slot, ms)) break;
+    if (ms <= best_ms) {
+      const I x = xo + xi;
+      if (ms < best_ms || x < bx) {
+        best_ms = ms;
+        bx = x;
+      }
+    }
+    // odometer step on the inner digits
+#pragma unroll
+    for (uint32_t j = 0; j < J; ++j) {
+      const uint32_t o = tab[kEnumOptBase + j];
+      const uint32_t d = (idig >> (2u * j)) & 3u;
+      const M b = M(1) << tab[kEnumLabBase + j];
+      const I w = I(uint64_t(tab[kEnumWeightBase + 2 * j]) |
+                    (uint64_t(tab[kEnumWeightBase + 2 * j + 1]) << 32));
+      ign &= ~b;
+      igq &= ~b;
+      const bool carry = d + 1u == opt_radix(o);
+      const uint32_t m = opt_mode(o, carry ? 0u : d + 1u);
+      if (m == 1u) ign |= b;
+      if (m == 2u) igq |= b;
+      if (!carry) {
+        idig += 1u << (2u * j);
+        xi += w;
+        break;
+      }
+      idig &= ~(3u << (2u * j));
+      xi -= I(d) * w;
+    }
+  }
+  if (best_ms != kInf) best_x = bx;
+}
+
 // Exhaustive search.  Block b serves table b / blocks_per_table and walks its
 // work items (kBlock consecutive outer combinations each) with a stride of
 // blocks_per_table.  Each lane keeps its own (makespan, index) minimum; the
@@ -679,6 +839,8 @@ template <int N, bool FULL, bool SHARE>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(SHARE ? DEVMAP_SHARE_WAVES : DEVMAP_SEARCH_WAVES))) void search_kernel(SearchArgs a) {
   __shared__ uint32_t s_lds[lds_words<N>()];
   __shared__ MaskT<N> s_wave[kBlock / 64];
+  constexpr bool kPrefix = FULL && !SHARE && N <= kPrefixMaxN;
+  __shared__ uint32_t s_snap[kPrefix ? snap_words<N>() * kBlock : 1];
   const uint32_t table = blockIdx.x / a.blocks_per_table;
   const uint32_t bb = blockIdx.x - table * a.blocks_per_table;
   const uint32_t* tab = a.tables + size_t(table) * a.table_stride;
@@ -686,9 +848,21 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(SHARE ? 
 
   uint32_t best_ms = kInf;
   uint64_t best_x = ~0ull;
-  for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-    lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x, &s_wave[threadIdx.x / 64],
-                                best_ms, best_x);
+  if constexpr (kPrefix) {
+    if (a.prefix) {
+      for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
+        lane_search_prefix<N>(a, tab, s_lds, item, threadIdx.x, &s_wave[threadIdx.x / 64],
+                              s_snap + threadIdx.x, best_ms, best_x);
+    } else {
+      for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
+        lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x,
+                                    &s_wave[threadIdx.x / 64], best_ms, best_x);
+    }
+  } else {
+    for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
+      lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x, &s_wave[threadIdx.x / 64],
+                                  best_ms, best_x);
+  }
 
   block_min(best_ms, best_x);
   if (threadIdx.x == 0) {
