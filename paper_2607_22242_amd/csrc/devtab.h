@@ -22,7 +22,10 @@ constexpr int kMaxLevels = 64;
 constexpr uint32_t kInf = 0xFFFFFFFFu;  // "never": unknown ready time, infeasible
 constexpr int kBlock = 256;             // threads per search block (4 waves)
 constexpr int kMaxInnerDigits = 6;      // inner (wave-uniform) digits per lane
-constexpr uint32_t kSharedInner = 3;    // inner digits of a shared-prefix search
+#ifndef DEVMAP_SHARED_INNER
+#define DEVMAP_SHARED_INNER 2
+#endif
+constexpr uint32_t kSharedInner = DEVMAP_SHARED_INNER;  // inner digits of a shared-prefix search
 constexpr int kPrefixMaxN = 24;         // tool counts served by shared prefixes
 
 // Header words.
