@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 14020097
-TRAFFIC_KERNEL_SHA256 = "eec48dea70041a6b03aa1909a1d6098cb5e67d442c58ab32734e1fbfdaaadba9"
+TRAFFIC_BYTES = 25752795
+TRAFFIC_KERNEL_SHA256 = "2ae0e5f38d7c299557e4e991e6fce1cf0ecba1f1a0fb0d91c897fb4933acd834"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 

@@ -559,9 +559,15 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
   }
 }
 
-// Waves per SIMD the search kernel is compiled for (the register budget).
-#ifndef DEVMAP_SEARCH_WAVES
-#define DEVMAP_SEARCH_WAVES 8
+// Waves per SIMD the search kernel is compiled for (the register budget):
+// 8 up to 16 tools, 6 beyond (measured: 6 waves take the 19-tool search from
+// 114 to 102 ms and the 32-tool one from 459 to 264 ms; the 14-tool batch
+// runs 10 % faster at 8).
+#ifndef DEVMAP_SEARCH_WAVES_SMALL
+#define DEVMAP_SEARCH_WAVES_SMALL 8
+#endif
+#ifndef DEVMAP_SEARCH_WAVES_LARGE
+#define DEVMAP_SEARCH_WAVES_LARGE 6
 #endif
 // The same for the processor-sharing evaluator, which keeps a 64-bit virtual
 // finish per tool.
@@ -685,8 +691,9 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // reuses after it, where other lanes are active.
 template <int N>
 constexpr uint32_t snap_words() {
-  // T of every tool, three masks, t, qfin, minq
-  return N <= kPrefixMaxN ? uint32_t(N) + 3u * (N > 32 ? 2u : 1u) + 3u : 1u;
+  // T of every tool, the done mask, t, qfin, minq (started and resolved
+  // follow from the tags of T)
+  return N <= kPrefixMaxN ? uint32_t(N) + (N > 32 ? 2u : 1u) + 3u : 1u;
 }
 
 template <int N>
@@ -711,8 +718,6 @@ __host__ __device__ __forceinline__ void snap_save(uint32_t* s, const Sim<N>& si
   uint32_t k = 0;
 #pragma unroll
   for (int i = 0; i < N; ++i) s[(k++) * kBlock] = sim.T[i];
-  snap_mask<N>(s, k, sim.started);
-  snap_mask<N>(s, k, sim.resolved);
   snap_mask<N>(s, k, sim.done);
   s[(k++) * kBlock] = sim.t;
   s[(k++) * kBlock] = sim.qfin;
@@ -724,8 +729,17 @@ __host__ __device__ __forceinline__ void snap_load(const uint32_t* s, Sim<N>& si
   uint32_t k = 0;
 #pragma unroll
   for (int i = 0; i < N; ++i) sim.T[i] = s[(k++) * kBlock];
-  sim.started = unsnap_mask<N>(s, k);
-  sim.resolved = unsnap_mask<N>(s, k);
+  // resolved: a known ready or finish time; started: a finish time (a GPU
+  // tool's untagged one or a CPU tool's)
+  MaskT<N> res = 0, sta = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const uint32_t x = sim.T[i];
+    res |= (x != 0u) ? MaskT<N>(1) << i : MaskT<N>(0);
+    sta |= (x - 1u < kH - 1u || x >= kTagCpu) ? MaskT<N>(1) << i : MaskT<N>(0);
+  }
+  sim.resolved = res;
+  sim.started = sta;
   sim.done = unsnap_mask<N>(s, k);
   sim.t = s[(k++) * kBlock];
   sim.qfin = s[(k++) * kBlock];
@@ -836,7 +850,10 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
 // blocks_per_table.  Each lane keeps its own (makespan, index) minimum; the
 // block's minimum goes to partials[b].
 template <int N, bool FULL, bool SHARE>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(SHARE ? DEVMAP_SHARE_WAVES : DEVMAP_SEARCH_WAVES))) void search_kernel(SearchArgs a) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
+    SHARE ? DEVMAP_SHARE_WAVES
+          : (N <= 16 ? DEVMAP_SEARCH_WAVES_SMALL : DEVMAP_SEARCH_WAVES_LARGE)))) void
+search_kernel(SearchArgs a) {
   __shared__ uint32_t s_lds[lds_words<N>()];
   __shared__ MaskT<N> s_wave[kBlock / 64];
   constexpr bool kPrefix = FULL && !SHARE && N <= kPrefixMaxN;
