@@ -618,3 +618,21 @@ def test_sharing_batch_and_wide(torch_cuda, O):
     Q = O.Problem.from_instance(inst, sharing=True)
     idx = np.random.default_rng(3).integers(0, P.n_mappings, 5000, dtype=np.uint64)
     np.testing.assert_array_equal(gpu_eval(torch_cuda, P, idx), Q.eval_many(idx))
+
+
+def test_shared_prefix_restarts_with_mixed_restart_passes(torch_cuda, O):
+    """Full-range searches whose lanes restart their inner combinations at
+    different passes, including lanes whose prefix alone is infeasible
+    (regression: a restore that read the wrong words of the saved state)."""
+    inst = synth.random_instance(4602, 7, "random", tight=True)
+    Q = O.Problem(inst["tools"], inst["edges"], inst["contention_q16"], inst["vram_budget_mib"])
+    for masks in ([1, 3, 7, 5, 6, 3, 7], [1, 2, 7, 5, 6, 3, 7], [1, 3, 1, 5, 6, 3, 7],
+                  [3] * 7, [7] * 7, [1, 7, 7, 7, 7, 7, 7], [7, 3, 7, 5, 6, 3, 7]):
+        P = S.Problem(inst["tools"], inst["edges"], inst["contention_q16"],
+                      inst["vram_budget_mib"], masks)
+        assert gpu_argmin(torch_cuda, P) == O.masked_argmin(Q, O.Space(masks)), masks
+    # and large enough for the shared-prefix plan (3^16 with a tight budget)
+    inst = synth.random_instance(4603, 16, "random", tight=True)
+    P, Q = both(inst, O)
+    say("shared-prefix plan, 3^16 tight")
+    assert gpu_argmin(torch_cuda, P) == Q.argmin()
