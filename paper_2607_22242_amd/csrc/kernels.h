@@ -222,8 +222,17 @@ struct Sim {
     const uint32_t lim = kH - t1;  // d = x - t1 < lim: x is a time after t
     const uint32_t now_t = kTagNow + t;
     // tools some lane of the wave has waiting or running / not resolved
-    const M wa = wave_or<M>(resolved & ~done, slot);
-    const M wu = wave_or<M>(ALL & ~resolved, slot);
+    M wa, wu;
+    if constexpr (N <= 32) {  // both masks in one 64-bit OR (the slot is 8 bytes)
+      const uint64_t both = wave_or<uint64_t>(
+          uint64_t(resolved & ~done) | (uint64_t(ALL & ~resolved) << 32),
+          reinterpret_cast<uint64_t*>(slot));
+      wa = M(both);
+      wu = M(both >> 32);
+    } else {
+      wa = wave_or<M>(resolved & ~done, slot);
+      wu = wave_or<M>(ALL & ~resolved, slot);
+    }
 
     // A. concurrency and VRAM at t, after releases and immediate starts
     uint32_t in_use = 0, k = 0;
@@ -855,7 +864,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
           : (N <= 16 ? DEVMAP_SEARCH_WAVES_SMALL : DEVMAP_SEARCH_WAVES_LARGE)))) void
 search_kernel(SearchArgs a) {
   __shared__ uint32_t s_lds[lds_words<N>()];
-  __shared__ MaskT<N> s_wave[kBlock / 64];
+  __shared__ uint64_t s_wave_words[kBlock / 64];  // one 8-byte word per wave
+  MaskT<N>* const slot = reinterpret_cast<MaskT<N>*>(&s_wave_words[threadIdx.x / 64]);
   constexpr bool kPrefix = FULL && !SHARE && N <= kPrefixMaxN;
   __shared__ uint32_t s_snap[kPrefix ? snap_words<N>() * kBlock : 1];
   const uint32_t table = blockIdx.x / a.blocks_per_table;
@@ -868,16 +878,16 @@ search_kernel(SearchArgs a) {
   if constexpr (kPrefix) {
     if (a.prefix) {
       for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-        lane_search_prefix<N>(a, tab, s_lds, item, threadIdx.x, &s_wave[threadIdx.x / 64],
+        lane_search_prefix<N>(a, tab, s_lds, item, threadIdx.x, slot,
                               s_snap + threadIdx.x, best_ms, best_x);
     } else {
       for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
         lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x,
-                                    &s_wave[threadIdx.x / 64], best_ms, best_x);
+                                    slot, best_ms, best_x);
     }
   } else {
     for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-      lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x, &s_wave[threadIdx.x / 64],
+      lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x, slot,
                                   best_ms, best_x);
   }
 
@@ -899,7 +909,8 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
                                                       int64_t* __restrict__ out) {
   using M = MaskT<N>;
   __shared__ uint32_t s_lds[lds_words<N>()];
-  __shared__ MaskT<N> s_wave[kBlock / 64];
+  __shared__ uint64_t s_wave_words[kBlock / 64];  // one 8-byte word per wave
+  MaskT<N>* const slot = reinterpret_cast<MaskT<N>*>(&s_wave_words[threadIdx.x / 64]);
   stage_tables<N>(tab, s_lds);
   const uint32_t levels = tab[kHdrLevels];
   const uint32_t budget = tab[kHdrBudget];
@@ -915,7 +926,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
       if constexpr (SHARE)
         ms = evaluate_sharing<N>(tab, s_lds, levels, budget, gn, gq);
       else
-        ms = evaluate<N>(tab, s_lds, levels, budget, gn, gq, &s_wave[threadIdx.x / 64]);
+        ms = evaluate<N>(tab, s_lds, levels, budget, gn, gq, slot);
       if (ms != kInf) r = int64_t(ms);
     }
     out[i] = r;
