@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 25752795
-TRAFFIC_KERNEL_SHA256 = "2ae0e5f38d7c299557e4e991e6fce1cf0ecba1f1a0fb0d91c897fb4933acd834"
+TRAFFIC_BYTES = 29676214
+TRAFFIC_KERNEL_SHA256 = "9d5bc74a9ff60852ee90c9ed162a47e81f45236c68ba044e6c84657b30e8846d"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 
