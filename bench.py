@@ -120,8 +120,8 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the search "
-              "shards by index range with one 16-byte reduction, which this build does not "
-              "launch.", file=sys.stderr)
+              "would shard by index range with one 16-byte reduction, which is not "
+              "implemented.", file=sys.stderr)
         sys.exit(2)
 
     import torch
