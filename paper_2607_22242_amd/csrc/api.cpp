@@ -504,7 +504,7 @@ void neighbourhood(const sched_problem& p, uint64_t base, std::vector<uint64_t>&
 // Exact search with pruning.
 
 constexpr uint64_t kPruneMinSpace = 1ull << 22;  // smaller spaces: one exhaustive search
-constexpr uint64_t kMaxPrefixes = 1ull << 20;    // bounded prefix assignments per call
+constexpr uint64_t kMaxPrefixes = 1ull << 24;    // bounded prefix assignments per call
 constexpr uint64_t kMinSubspace = 1ull << 12;    // mappings per searched subspace, at least
 constexpr uint32_t kChunkTables = 2048;          // subspaces per search launch
 
@@ -556,7 +556,9 @@ PruneLayout prune_layout(const sched_problem& p, const PrunePlan& pl) {
   l.partials = align_up(size_t(kChunkTables) * p.table_words * 4);
   l.results = l.partials + align_up(partial_capacity(kChunkTables) * sizeof(Partial));
   l.bounds = l.results + align_up(size_t(kChunkTables) * sizeof(DevResult));
-  l.probe_idx = l.bounds + align_up(size_t(pl.n_prefixes) * 4);
+  // Survivor count (one word, padded) and then up to n_prefixes (bound, y)
+  // pairs.
+  l.probe_idx = l.bounds + align_up(4) + align_up(size_t(pl.n_prefixes) * 8);
   l.probe_ms = l.probe_idx + align_up(probes * 8);
   l.total = l.probe_ms + align_up(probes * 8);
   return l;
@@ -953,21 +955,28 @@ int sched_pruned_argmin(const sched_problem* p, void* d_workspace, size_t ws_byt
       if (p->radix[v] == 1) known |= 1ull << p->table[kPosBase + v];
     HIP_TRY(hipMemcpyAsync(ws + L.tables, btab.data(), size_t(stride) * 4, hipMemcpyHostToDevice,
                            s));
-    uint32_t* d_bounds = reinterpret_cast<uint32_t*>(ws + L.bounds);
-    HIP_TRY(launch_bound(n, d_tab, uint32_t(pl.prefix.size()), known, int64_t(pl.n_prefixes),
-                         d_bounds, s));
-    std::vector<uint32_t> lb(pl.n_prefixes);
-    HIP_TRY(hipMemcpyAsync(lb.data(), d_bounds, pl.n_prefixes * 4, hipMemcpyDeviceToHost, s));
+    uint32_t* d_count = reinterpret_cast<uint32_t*>(ws + L.bounds);
+    uint2* d_live = reinterpret_cast<uint2*>(ws + L.bounds + align_up(4));
+    const uint32_t ub32 = ub_ms == INT64_MAX ? kInf - 1 : uint32_t(ub_ms);
+    HIP_TRY(hipMemsetAsync(d_count, 0, 4, s));
+    HIP_TRY(launch_bound(n, d_tab, uint32_t(pl.prefix.size()), known, int64_t(pl.n_prefixes), ub32,
+                         d_count, d_live, s));
+    uint32_t n_live = 0;
+    HIP_TRY(hipMemcpyAsync(&n_live, d_count, 4, hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
+    if (n_live > pl.n_prefixes) return SCHED_E_DEVICE;
+    std::vector<uint2> raw(n_live);
+    if (n_live) {
+      HIP_TRY(hipMemcpyAsync(raw.data(), d_live, size_t(n_live) * 8, hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipStreamSynchronize(s));
+    }
     st.prefixes = pl.n_prefixes;
     st.prefix_tools = int32_t(pl.prefix.size());
 
     // Survivors: bound <= upper bound (equal bounds may hide a lower index),
-    // most promising first.
-    std::vector<std::pair<uint32_t, uint64_t>> live;
-    for (uint64_t y = 0; y < pl.n_prefixes; ++y)
-      if (lb[y] != kInf && (ub_ms == INT64_MAX || int64_t(lb[y]) <= ub_ms))
-        live.push_back({lb[y], y});
+    // most promising first; the kernel appends them in no fixed order.
+    std::vector<std::pair<uint32_t, uint64_t>> live(n_live);
+    for (uint32_t i = 0; i < n_live; ++i) live[i] = {raw[i].x, raw[i].y};
     std::sort(live.begin(), live.end());
 
     // 3. Subspaces: the prefix tools fixed, the rest enumerated with the

@@ -18,7 +18,7 @@ hipError_t launch_eval_n(const uint32_t* tab, const uint64_t* idx, int64_t n, ui
                          int64_t* out, uint32_t sharing, hipStream_t s);
 template <int N>
 hipError_t launch_bound_n(const uint32_t* tab, uint32_t K, uint64_t known, int64_t n,
-                          uint32_t* out, hipStream_t s);
+                          uint32_t ub, uint32_t* count, uint2* out, hipStream_t s);
 
 __device__ __forceinline__ void lex_min(uint32_t& ms, uint64_t& x, uint32_t oms, uint64_t ox) {
   if (oms < ms || (oms == ms && ox < x)) {
@@ -77,8 +77,8 @@ template <size_t... I>
 static constexpr auto make_eval_table(std::index_sequence<I...>) {
   return std::array<EvalFn, sizeof...(I)>{&launch_eval_n<int(I) + 1>...};
 }
-using BoundFn = hipError_t (*)(const uint32_t*, uint32_t, uint64_t, int64_t, uint32_t*,
-                               hipStream_t);
+using BoundFn = hipError_t (*)(const uint32_t*, uint32_t, uint64_t, int64_t, uint32_t, uint32_t*,
+                               uint2*, hipStream_t);
 template <size_t... I>
 static constexpr auto make_bound_table(std::index_sequence<I...>) {
   return std::array<BoundFn, sizeof...(I)>{&launch_bound_n<int(I) + 1>...};
@@ -98,8 +98,8 @@ hipError_t launch_eval(int n_tools, const uint32_t* tab, const uint64_t* idx, in
 }
 
 hipError_t launch_bound(int n_tools, const uint32_t* tab, uint32_t K, uint64_t known, int64_t n,
-                        uint32_t* out, hipStream_t s) {
-  return kBoundFns[n_tools - 1](tab, K, known, n, out, s);
+                        uint32_t ub, uint32_t* count, uint2* out, hipStream_t s) {
+  return kBoundFns[n_tools - 1](tab, K, known, n, ub, count, out, s);
 }
 
 hipError_t launch_reduce(const Partial* partials, uint32_t per_table, uint32_t n_tables,

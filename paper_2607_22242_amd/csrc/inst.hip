@@ -14,7 +14,7 @@ namespace devmap {
   template hipError_t launch_eval_n<N>(const uint32_t*, const uint64_t*, int64_t, \
                                        uint64_t, int64_t*, uint32_t, hipStream_t); \
   template hipError_t launch_bound_n<N>(const uint32_t*, uint32_t, uint64_t, int64_t, \
-                                        uint32_t*, hipStream_t);
+                                        uint32_t, uint32_t*, uint2*, hipStream_t);
 
 #if INST_LO <= 1 && 1 <= INST_HI
 DEVMAP_INST(1)

@@ -975,17 +975,24 @@ __host__ __device__ __forceinline__ uint32_t prefix_bound(const uint32_t* __rest
 
 // Bounds of prefixes [0, n): prefix y holds the mixed-radix digits of the
 // table's enumeration positions [0, K); known = the labels of those tools
-// and of the tools with a single allowed mode.
+// and of the tools with a single allowed mode.  Prefixes whose bound does
+// not exceed ub are appended to out as (bound, y) pairs; *count (zero on
+// entry) receives their number.  out holds n pairs, so none is lost.
 template <int N>
 __global__ __launch_bounds__(kBlock) void bound_kernel(const uint32_t* __restrict__ tab,
                                                        uint32_t K, uint64_t known, int64_t n,
-                                                       uint32_t* __restrict__ out) {
+                                                       uint32_t ub, uint32_t* __restrict__ count,
+                                                       uint2* __restrict__ out) {
   for (int64_t y = int64_t(blockIdx.x) * kBlock + threadIdx.x; y < n;
        y += int64_t(gridDim.x) * kBlock) {
     MaskT<N> gn, gq;
     uint64_t x;
     decode_positions<N>(tab, uint64_t(y), 0, K, gn, gq, x);
-    out[y] = prefix_bound<N>(tab, gn, gq, MaskT<N>(known));
+    const uint32_t lb = prefix_bound<N>(tab, gn, gq, MaskT<N>(known));
+    if (lb != kInf && lb <= ub) {
+      const uint32_t slot = atomicAdd(count, 1u);
+      out[slot] = make_uint2(lb, uint32_t(y));
+    }
   }
 }
 
@@ -1010,12 +1017,12 @@ hipError_t launch_search_n(const SearchArgs& a, hipStream_t s) {
 
 template <int N>
 hipError_t launch_bound_n(const uint32_t* tab, uint32_t K, uint64_t known, int64_t n,
-                          uint32_t* out, hipStream_t s) {
+                          uint32_t ub, uint32_t* count, uint2* out, hipStream_t s) {
   int64_t blocks = (n + kBlock - 1) / kBlock;
   if (blocks > 65536) blocks = 65536;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(bound_kernel<N>, dim3(uint32_t(blocks)), dim3(kBlock), 0, s, tab, K, known,
-                     n, out);
+                     n, ub, count, out);
   return hipGetLastError();
 }
 

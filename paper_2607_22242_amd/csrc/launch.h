@@ -10,7 +10,7 @@ hipError_t launch_search(int n_tools, const SearchArgs& a, hipStream_t s);
 hipError_t launch_eval(int n_tools, const uint32_t* tab, const uint64_t* idx, int64_t n,
                        uint64_t n_mappings, int64_t* out, uint32_t sharing, hipStream_t s);
 hipError_t launch_bound(int n_tools, const uint32_t* tab, uint32_t K, uint64_t known, int64_t n,
-                        uint32_t* out, hipStream_t s);
+                        uint32_t ub, uint32_t* count, uint2* out, hipStream_t s);
 hipError_t launch_reduce(const Partial* partials, uint32_t per_table, uint32_t n_tables,
                          DevResult* out, hipStream_t s);
 
