@@ -132,6 +132,33 @@ __host__ __device__ __forceinline__ M wave_or(M x, M* slot) {
 #endif
 }
 
+// Wave-wide OR of three per-lane tool masks through the calling wave's 8-byte
+// LDS slot: one 64-bit OR when 3N bits fit, else one per mask (or pair).
+template <int N>
+__host__ __device__ __forceinline__ void wave_or3(MaskT<N> a, MaskT<N> b, MaskT<N> c,
+                                                  MaskT<N>* slot, MaskT<N>& oa, MaskT<N>& ob,
+                                                  MaskT<N>& oc) {
+  using M = MaskT<N>;
+  uint64_t* const s64 = reinterpret_cast<uint64_t*>(slot);
+  if constexpr (3 * N <= 64) {
+    constexpr uint64_t m = (uint64_t(1) << N) - 1u;
+    const uint64_t r = wave_or<uint64_t>(uint64_t(a) | (uint64_t(b) << N) | (uint64_t(c) << (2 * N)),
+                                         s64);
+    oa = M(r & m);
+    ob = M((r >> N) & m);
+    oc = M((r >> (2 * N)) & m);
+  } else if constexpr (N <= 32) {
+    const uint64_t r = wave_or<uint64_t>(uint64_t(a) | (uint64_t(b) << 32), s64);
+    oa = M(r);
+    ob = M(r >> 32);
+    oc = wave_or<uint64_t>(uint64_t(c), s64);
+  } else {
+    oa = wave_or<M>(a, slot);
+    ob = wave_or<M>(b, slot);
+    oc = wave_or<M>(c, slot);
+  }
+}
+
 // Event-driven schedule of one mapping (the schedule model in full), advanced
 // one event time per call of step().
 //
@@ -154,19 +181,24 @@ __host__ __device__ __forceinline__ M wave_or(M x, M* slot) {
 // one event time t:
 //   A. GPU tools running at t plus gpu_now tools ready at t give the
 //      concurrency k and the VRAM in use (over the budget: out of memory);
-//      if no queued tool is running, the ready queued tool with the smallest
-//      (ready time, original number) is admitted when it fits;
+//      if no queued tool is running and one is ready, the queue head -- the
+//      lowest original number among the queued tools ready at minq, the
+//      earliest ready time -- is admitted when it fits;
 //   B. in label order: starters get f = t + dur[k], fixed for their life;
 //      tools whose predecessors have all started get their ready time
 //      r = max over u -> i of finish(u) (+ xfer_i across devices); and the
-//      next event is accumulated: gpu_now and gpu_queue ready times after t,
-//      plus GPU finishes when a ready queued tool is still waiting (only the
-//      queue's own finish when the queue is busy).
-// Work is skipped for tools that are settled in every lane of the wave: a
-// pass only visits tools that some lane still has waiting or running (the
-// wave-wide OR of the lanes' active masks) and, for resolution, tools that
-// some lane has not resolved yet.  A settled tool contributes nothing to a
-// pass, so skipping it changes no result.
+//      next event is chosen: the next gpu_now ready time, and while a ready
+//      queued tool waits, the queue's finish (busy queue) or the next GPU
+//      finish (VRAM); otherwise the next queued ready time.  While the head
+//      waits, a later queued arrival cannot move it, so that time is no
+//      event (visiting it would change nothing).
+// A pass visits a tool only where some lane of the wave needs it, by the
+// tool's state there: waiting (resolved, not started), running (a GPU tool
+// running at the previous event, or started there) or unresolved -- three
+// wave-wide ORs.  The work of a tool in any other state would change
+// nothing, so skipping it changes no result.  A tool's next-event
+// contribution is taken where its time becomes known (its start or its
+// resolution) or from its state.
 // A mapping needs at most 2N+1 passes: every pass after the first moves t to
 // a ready or finish time, and each tool has one of each.
 constexpr uint32_t kH = 0x40000000u;  // 2^30: time limit and tag unit
@@ -181,7 +213,7 @@ struct Sim {
   M gnm, gqm;
   M started;   // started GPU tools and resolved CPU tools
   M resolved;  // tools whose ready time is known
-  M done;      // CPU tools and GPU tools seen finished
+  M run;       // GPU tools running at the last pass's t or started there
   uint32_t t;
   uint32_t qfin;  // finish of the running queued tool (0: none)
   uint32_t minq;  // earliest ready time of a waiting queued tool (>= H: none)
@@ -194,7 +226,7 @@ struct Sim {
     for (int i = 0; i < N; ++i) T[i] = 0;
     started = 0;
     resolved = 0;
-    done = 0;
+    run = 0;
     t = 0;
     qfin = 0;
     minq = kInf;
@@ -221,80 +253,82 @@ struct Sim {
     const uint32_t t1 = t + 1u;
     const uint32_t lim = kH - t1;  // d = x - t1 < lim: x is a time after t
     const uint32_t now_t = kTagNow + t;
-    // tools some lane of the wave has waiting or running / not resolved
-    M wa, wu;
-    if constexpr (N <= 32) {  // both masks in one 64-bit OR (the slot is 8 bytes)
-      const uint64_t both = wave_or<uint64_t>(
-          uint64_t(resolved & ~done) | (uint64_t(ALL & ~resolved) << 32),
-          reinterpret_cast<uint64_t*>(slot));
-      wa = M(both);
-      wu = M(both >> 32);
-    } else {
-      wa = wave_or<M>(resolved & ~done, slot);
-      wu = wave_or<M>(ALL & ~resolved, slot);
-    }
+    // tools some lane of the wave has waiting / running / unresolved
+    M ww, wr, wu;
+    wave_or3<N>(resolved & ~started, run, ALL & ~resolved, slot, ww, wr, wu);
 
-    // A. concurrency and VRAM at t, after releases and immediate starts
-    uint32_t in_use = 0, k = 0;
+    // A. concurrency and VRAM at t, after releases and immediate starts; the
+    // earliest finish after t of a running tool
+    uint32_t in_use = 0, k = 0, tf = kInf;
+    run = 0;
+    const M wr_a = opaque(wr);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      if ((wa >> i) & 1) {
-        const uint32_t x = T[i];
-        const bool on = (x - t1 < lim) | (x == now_t);
-        in_use += on ? tp[kHdrWords + kToolWords * i + kToolMem] : 0u;
+      if ((wr_a >> i) & 1) {
+        DEVMAP_KEEP_BRANCH();
+        const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
+        const uint32_t d = T[i] - t1;
+        const bool on = d < lim;  // finishes after t
+        in_use += on ? mem : 0u;
         k += on ? 1u : 0u;
-        if (x - 1u < t) done |= M(1) << i;  // a GPU tool finished by t
+        run |= on ? M(1) << i : M(0);
+        tf = umin32(tf, d);
+      }
+    }
+    const M ww_a = opaque(ww);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if ((ww_a >> i) & 1) {
+        DEVMAP_KEEP_BRANCH();
+        const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
+        const bool on = T[i] == now_t;  // gpu_now, ready at t
+        in_use += on ? mem : 0u;
+        k += on ? 1u : 0u;
       }
     }
     if (in_use > budget) return true;  // out of memory: infeasible
     uint32_t hsel = kInf;              // label of the queued tool admitted at t
-    uint32_t waiting = 0;              // ready queued tools left waiting
-    if (minq <= t) {
-      if (qfin <= t) {
-        uint32_t hR = kInf;
-        const M wa_q = opaque(wa);
+    if (minq <= t && qfin <= t) {
+      // the queue head: ready at minq (the earliest), lowest original number
+      const uint32_t key = kTagQueue + minq;
+      uint32_t hO = kInf;
+      const M ww_q = opaque(ww);
 #pragma unroll
-        for (int i = 0; i < N; ++i) {
-          if ((wa_q >> i) & 1) {
-            const uint32_t rq = T[i] - kTagQueue;  // a queued tool's ready time; others wrap high
-            const bool rd = rq <= t;
-            waiting += rd ? 1u : 0u;
-            hR = umin32(hR, rd ? rq : kInf);
-          }
+      for (int i = 0; i < N; ++i) {
+        if ((ww_q >> i) & 1) {
+          DEVMAP_KEEP_BRANCH();
+          const uint32_t orig = opaque(tp[kHdrWords + kToolWords * i + kToolOrig]);
+          hO = T[i] == key ? umin32(hO, orig) : hO;
         }
-        uint32_t hO = kInf;  // FIFO ties go to the lowest original number
-        const M wa_t = opaque(wa);
-#pragma unroll
-        for (int i = 0; i < N; ++i)
-          if ((wa_t >> i) & 1)
-            hO = umin32(hO, T[i] - kTagQueue == hR ? tp[kHdrWords + kToolWords * i + kToolOrig]
-                                                    : kInf);
-        const uint32_t lab = s_pos[hO];
-        if (s_mem[lab] <= budget - in_use) {
-          hsel = lab;
-          k += 1;
-          waiting -= 1;
-        }
-      } else {
-        waiting = 1;  // the queue is busy; its finish is the next chance
+      }
+      const uint32_t lab = s_pos[hO];
+      if (s_mem[lab] <= budget - in_use) {
+        hsel = lab;
+        k += 1;
       }
     }
     const uint32_t lev = umin32(umax32(k, 1u), levels) - 1u;
 
     // B. starts, resolution, next event
-    uint32_t tn = kInf, tq = kInf, tf = kInf;
+    uint32_t tn = kInf;
     minq = kInf;
-    const M wa_b = opaque(wa), wu_b = opaque(wu);
+    const M ww_b = opaque(ww), wu_b = opaque(wu);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       const M bi = M(1) << i;
-      if ((wa_b >> i) & 1) {
+      if ((ww_b >> i) & 1) {
         const bool adm = (hsel == uint32_t(i));
         if (T[i] == now_t || adm) {
-          T[i] = t + s_dur[(uint32_t(i) * 2u + (adm ? 1u : 0u)) * levels + lev];
+          const uint32_t d = s_dur[(uint32_t(i) * 2u + (adm ? 1u : 0u)) * levels + lev];
+          T[i] = t + d;
           started |= bi;
+          run |= bi;
+          tf = umin32(tf, d - 1u);  // finish after t
           if (adm) qfin = T[i];
         }
+        const uint32_t x = T[i];
+        tn = umin32(tn, x - kTagNow - t1);     // gpu_now ready after t
+        minq = umin32(minq, x - kTagQueue);   // queued ready time (>= H: none)
       }
       if ((wu_b >> i) & 1) {
         const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
@@ -319,19 +353,14 @@ struct Sim {
           if (!on_gpu) {
             T[i] = kTagCpu + r + rec[kToolCpu];
             started |= bi;
-            done |= bi;
+          } else if (gnm & bi) {
+            T[i] = kTagNow + r;
+            tn = umin32(tn, r - t1);
           } else {
-            T[i] = ((gnm & bi) ? kTagNow : kTagQueue) + r;
+            T[i] = kTagQueue + r;
+            minq = umin32(minq, r);
           }
         }
-      }
-      if (((wa_b | wu_b) >> i) & 1) {
-        const uint32_t x = T[i];
-        tn = umin32(tn, x - kTagNow - t1);     // gpu_now ready after t
-        const uint32_t rq = x - kTagQueue;
-        minq = umin32(minq, rq);               // queued ready time (>= H: none)
-        tq = umin32(tq, rq - t1);              // queued ready after t
-        tf = umin32(tf, x - t1);               // GPU finish after t
       }
     }
     if (started == ALL) {
@@ -344,13 +373,16 @@ struct Sim {
     if (pass == 0) return false;  // sources resolved: now the events at t = 0
     uint32_t next = kInf;
     if (tn < lim) next = tn + t1;
-    if (tq < lim) next = umin32(next, tq + t1);
-    if (waiting != 0) {
+    if (minq <= t) {
+      // A ready queued tool is still waiting: the queue head can only move
+      // when the queue frees or VRAM is released, whatever else turns ready.
       if (qfin > t) {
         next = umin32(next, qfin);     // queue busy: wait for it
       } else if (tf < lim) {
         next = umin32(next, tf + t1);  // blocked on VRAM: wait for a release
       }
+    } else if (minq < kH) {
+      next = umin32(next, minq);       // the next queued tool turns ready
     }
     if (next == kInf) return true;  // a queued tool can never fit: infeasible
     t = next;
@@ -700,7 +732,7 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // reuses after it, where other lanes are active.
 template <int N>
 constexpr uint32_t snap_words() {
-  // T of every tool, the done mask, t, qfin, minq (started and resolved
+  // T of every tool, the run mask, t, qfin, minq (started and resolved
   // follow from the tags of T)
   return N <= kPrefixMaxN ? uint32_t(N) + (N > 32 ? 2u : 1u) + 3u : 1u;
 }
@@ -727,7 +759,7 @@ __host__ __device__ __forceinline__ void snap_save(uint32_t* s, const Sim<N>& si
   uint32_t k = 0;
 #pragma unroll
   for (int i = 0; i < N; ++i) s[(k++) * kBlock] = sim.T[i];
-  snap_mask<N>(s, k, sim.done);
+  snap_mask<N>(s, k, sim.run);
   s[(k++) * kBlock] = sim.t;
   s[(k++) * kBlock] = sim.qfin;
   s[(k++) * kBlock] = sim.minq;
@@ -749,7 +781,7 @@ __host__ __device__ __forceinline__ void snap_load(const uint32_t* s, Sim<N>& si
   }
   sim.resolved = res;
   sim.started = sta;
-  sim.done = unsnap_mask<N>(s, k);
+  sim.run = unsnap_mask<N>(s, k);
   sim.t = s[(k++) * kBlock];
   sim.qfin = s[(k++) * kBlock];
   sim.minq = s[(k++) * kBlock];
