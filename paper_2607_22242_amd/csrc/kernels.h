@@ -217,6 +217,7 @@ struct Sim {
   uint32_t t;
   uint32_t qfin;  // finish of the running queued tool (0: none)
   uint32_t minq;  // earliest ready time of a waiting queued tool (>= H: none)
+  uint32_t mk;    // latest finish of the started tools
   bool dead;      // statically infeasible
 
   __host__ __device__ __forceinline__ void init(const uint32_t* __restrict__ tab, M gn, M gq) {
@@ -230,6 +231,7 @@ struct Sim {
     t = 0;
     qfin = 0;
     minq = kInf;
+    mk = 0;
     // a GPU mode whose footprint exceeds the budget never fits
     dead = ((gn | gq) & load_mask<N>(Tab{tab}, kHdrBigLo)) != 0;
   }
@@ -270,10 +272,14 @@ struct Sim {
         const uint32_t d = T[i] - t1;
         const bool on = d < lim;  // finishes after t
         in_use += on ? mem : 0u;
-        k += on ? 1u : 0u;
         run |= on ? M(1) << i : M(0);
         tf = umin32(tf, d);
       }
+    }
+    if constexpr (N <= 32) {
+      k = __builtin_popcount(uint32_t(run));
+    } else {
+      k = __builtin_popcountll(uint64_t(run));
     }
     const M ww_a = opaque(ww);
 #pragma unroll
@@ -324,6 +330,7 @@ struct Sim {
           started |= bi;
           run |= bi;
           tf = umin32(tf, d - 1u);  // finish after t
+          mk = umax32(mk, T[i]);
           if (adm) qfin = T[i];
         }
         const uint32_t x = T[i];
@@ -351,8 +358,10 @@ struct Sim {
           const uint32_t r = on_gpu ? umax32(g, c ? c + xw : 0u) : umax32(c, g ? g + xw : 0u);
           resolved |= bi;
           if (!on_gpu) {
-            T[i] = kTagCpu + r + rec[kToolCpu];
+            const uint32_t f = r + rec[kToolCpu];
+            T[i] = kTagCpu + f;
             started |= bi;
+            mk = umax32(mk, f);
           } else if (gnm & bi) {
             T[i] = kTagNow + r;
             tn = umin32(tn, r - t1);
@@ -364,10 +373,7 @@ struct Sim {
       }
     }
     if (started == ALL) {
-      uint32_t m = 0;
-#pragma unroll
-      for (int i = 0; i < N; ++i) m = umax32(m, T[i] & (kH - 1u));
-      ms = m;
+      ms = mk;
       return true;
     }
     if (pass == 0) return false;  // sources resolved: now the events at t = 0
@@ -724,67 +730,51 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // schedule of the other tools, and every event time, is the same for all
 // their modes: each lane runs that prefix once per outer combination, keeps
 // the state it had before the first pass that resolves an inner tool, and
-// restarts every inner combination from there.  The state goes to LDS (one
-// column per lane), so it costs no registers.  Tools up to kPrefixMaxN.
+// restarts every inner combination from there.  The per-tool words go to LDS
+// (one column per lane), the three masks to registers.  Tools up to
+// kPrefixMaxN.
 // Every tool's word is saved and restored, inner tools included (they are
 // 0): a branch per tool on the wave-uniform inner mask would be compiled as a
 // lane-mask test that the compiler computes inside the prefix loop and
 // reuses after it, where other lanes are active.
 template <int N>
 constexpr uint32_t snap_words() {
-  // T of every tool, the run mask, t, qfin, minq (started and resolved
-  // follow from the tags of T)
-  return N <= kPrefixMaxN ? uint32_t(N) + (N > 32 ? 2u : 1u) + 3u : 1u;
+  // T of every tool, t, qfin, minq, mk (the masks stay in registers)
+  return N <= kPrefixMaxN ? uint32_t(N) + 4u : 1u;
 }
 
+// A lane's saved schedule state: the words in its LDS column s, the masks in
+// registers.
 template <int N>
-__host__ __device__ __forceinline__ void snap_mask(uint32_t* s, uint32_t& k, MaskT<N> m) {
-  s[(k++) * kBlock] = uint32_t(m);
-  if constexpr (N > 32) s[(k++) * kBlock] = uint32_t(uint64_t(m) >> 32);
-}
+struct Snap {
+  MaskT<N> started, resolved, run;
+};
 
 template <int N>
-__host__ __device__ __forceinline__ MaskT<N> unsnap_mask(const uint32_t* s, uint32_t& k) {
-  if constexpr (N > 32) {
-    const uint64_t lo = s[(k++) * kBlock];
-    return lo | (uint64_t(s[(k++) * kBlock]) << 32);
-  } else {
-    return s[(k++) * kBlock];
-  }
-}
-
-// Save / restore a lane's schedule state.  s: this lane's column.
-template <int N>
-__host__ __device__ __forceinline__ void snap_save(uint32_t* s, const Sim<N>& sim) {
-  uint32_t k = 0;
+__host__ __device__ __forceinline__ void snap_save(uint32_t* s, Snap<N>& m, const Sim<N>& sim) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) s[(k++) * kBlock] = sim.T[i];
-  snap_mask<N>(s, k, sim.run);
-  s[(k++) * kBlock] = sim.t;
-  s[(k++) * kBlock] = sim.qfin;
-  s[(k++) * kBlock] = sim.minq;
+  for (int i = 0; i < N; ++i) s[i * kBlock] = sim.T[i];
+  s[(N + 0) * kBlock] = sim.t;
+  s[(N + 1) * kBlock] = sim.qfin;
+  s[(N + 2) * kBlock] = sim.minq;
+  s[(N + 3) * kBlock] = sim.mk;
+  m.started = sim.started;
+  m.resolved = sim.resolved;
+  m.run = sim.run;
 }
 
 template <int N>
-__host__ __device__ __forceinline__ void snap_load(const uint32_t* s, Sim<N>& sim) {
-  uint32_t k = 0;
+__host__ __device__ __forceinline__ void snap_load(const uint32_t* s, const Snap<N>& m,
+                                                   Sim<N>& sim) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) sim.T[i] = s[(k++) * kBlock];
-  // resolved: a known ready or finish time; started: a finish time (a GPU
-  // tool's untagged one or a CPU tool's)
-  MaskT<N> res = 0, sta = 0;
-#pragma unroll
-  for (int i = 0; i < N; ++i) {
-    const uint32_t x = sim.T[i];
-    res |= (x != 0u) ? MaskT<N>(1) << i : MaskT<N>(0);
-    sta |= (x - 1u < kH - 1u || x >= kTagCpu) ? MaskT<N>(1) << i : MaskT<N>(0);
-  }
-  sim.resolved = res;
-  sim.started = sta;
-  sim.run = unsnap_mask<N>(s, k);
-  sim.t = s[(k++) * kBlock];
-  sim.qfin = s[(k++) * kBlock];
-  sim.minq = s[(k++) * kBlock];
+  for (int i = 0; i < N; ++i) sim.T[i] = s[i * kBlock];
+  sim.t = s[(N + 0) * kBlock];
+  sim.qfin = s[(N + 1) * kBlock];
+  sim.minq = s[(N + 2) * kBlock];
+  sim.mk = s[(N + 3) * kBlock];
+  sim.started = m.started;
+  sim.resolved = m.resolved;
+  sim.run = m.run;
 }
 
 // lane_search for a full range with shared prefixes (see above); the inner
@@ -816,11 +806,12 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
   // The prefix: inner tools on the CPU (their modes are never read before
   // one of them is resolved).  pstar: the first pass that resolves one.
   int pstar = -1;
+  Snap<N> sm;
   {
     Sim<N> sim;
     sim.init(tab, ogn, ogq);
     for (int pass = 0; pass < 2 * N + 2; ++pass) {
-      snap_save<N>(snap, sim);
+      snap_save<N>(snap, sm, sim);
       uint32_t ms;
       const bool fin = sim.step(tab, lds, levels, budget, pass, slot, ms);
       if (sim.resolved & inner) {
@@ -846,7 +837,7 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
   }
   for (uint32_t i = 0; i < a.inner_count; ++i) {
     Sim<N> sim;
-    snap_load<N>(snap, sim);
+    snap_load<N>(snap, sm, sim);
     sim.gnm = ogn | ign;
     sim.gqm = ogq | igq;
     sim.dead = ((sim.gnm | sim.gqm) & big) != 0;
