@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 29676214
-TRAFFIC_KERNEL_SHA256 = "9d5bc74a9ff60852ee90c9ed162a47e81f45236c68ba044e6c84657b30e8846d"
+TRAFFIC_BYTES = 15247360
+TRAFFIC_KERNEL_SHA256 = "5c86fd2b00014d3f8cfb513f28851ed9be92c937e8947e4b8fd579e9abd8eafe"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 
