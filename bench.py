@@ -53,6 +53,26 @@ def kernel_sha256() -> str:
     return h.hexdigest()
 
 
+def valu_ceiling(S, torch, stream, achieved: float) -> dict:
+    """Empirical integer VALU ceiling: the library's throughput probe (8
+    independent add/max/compare/select chains per lane, 2^13 blocks of 256),
+    timed with HIP events on the search's stream."""
+    blocks, iters = 8192, 30000
+    out = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+    S.sched_valu_probe(blocks, iters, out, stream)
+    torch.cuda.synchronize()
+    ms, ops = [], 0.0
+    for _ in range(3):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        ops = S.sched_valu_probe(blocks, iters, out, stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms.append(a.elapsed_time(b))
+    ceiling = ops / (sorted(ms)[1] / 1e3)
+    return {"ceiling": ceiling / 1e12, "ceiling_frac": achieved / ceiling}
+
+
 def algorithmic_ops_per_mapping(n_tools: int, n_edges: int) -> float:
     """Primitive int32 operations of one event-driven evaluation of a mapping.
 
@@ -234,6 +254,8 @@ def main():
                 "ops_per_mapping": ops, "kernel_ms": avg_launch_s * 1e3}
     if args.mode != "search":
         roofline = None  # several kernels and host steps per call: no single roofline
+    else:
+        roofline.update(valu_ceiling(S, torch, stream, achieved))
     if args.random_tools:
         workloads[args.config] = (f"random{args.random_tools}: random DAG "
                                   f"({len(inst['edges'])} edges), seed {args.random_seed}"

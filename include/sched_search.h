@@ -264,6 +264,18 @@ int sched_monitor_averages(const sched_monitor *m, int64_t *mean_us, int32_t *co
  * factor on top. */
 int sched_monitor_latencies(const sched_monitor *m, const sched_tool *profile, sched_lat *out);
 
+/* Diagnostic, not part of the method: the integer VALU throughput probe that
+ * gives the search's roofline an empirical ceiling next to the published
+ * peak.  Launches `blocks` blocks of 256 lanes on hip_stream; every lane runs
+ * `iters` steps of 8 independent chains of an add, a max, a compare and a
+ * select (32 int32 VALU operations per step) and writes one word of d_out
+ * (device, at least blocks * 256 uint32).  *lane_ops (host) receives the
+ * int32 lane operations of the launch.  Waits for the stream before
+ * returning.  Errors: SCHED_E_NULL (d_out or lane_ops null), SCHED_E_SIZE
+ * (blocks or iters 0, blocks > 2^24), SCHED_E_DEVICE. */
+int sched_valu_probe(uint32_t blocks, uint32_t iters, uint32_t *d_out, void *hip_stream,
+                     double *lane_ops);
+
 /* Static text for an error code. */
 const char *sched_strerror(int code);
 

@@ -30,7 +30,8 @@ EXPORTED = ["sched_problem_create", "sched_problem_create_masked", "sched_proble
             "sched_eval_batch", "sched_eval_mappings", "sched_eval_reprobes",
             "sched_pruned_workspace_bytes", "sched_pruned_argmin",
             "sched_monitor_create", "sched_monitor_destroy", "sched_monitor_observe",
-            "sched_monitor_averages", "sched_monitor_latencies", "sched_strerror"]
+            "sched_monitor_averages", "sched_monitor_latencies", "sched_valu_probe",
+            "sched_strerror"]
 
 
 class sched_tool(ctypes.Structure):
@@ -142,6 +143,9 @@ def lib():
         L.sched_monitor_averages.argtypes = [P, P, P]
         L.sched_monitor_latencies.restype = ctypes.c_int
         L.sched_monitor_latencies.argtypes = [P, P, P]
+        L.sched_valu_probe.restype = ctypes.c_int
+        L.sched_valu_probe.argtypes = [ctypes.c_uint32, ctypes.c_uint32, P, P,
+                                       ctypes.POINTER(ctypes.c_double)]
         L.sched_strerror.restype = ctypes.c_char_p
         L.sched_strerror.argtypes = [ctypes.c_int]
         _lib = L
@@ -293,6 +297,16 @@ def sched_eval_mappings(handle, d_idx, d_makespan, workspace, stream=None) -> No
     wp, wb = _ws(workspace)
     _check(lib().sched_eval_mappings(handle, d_idx.data_ptr(), n, d_makespan.data_ptr(), wp, wb,
                                      _stream_ptr(stream)), "sched_eval_mappings")
+
+
+def sched_valu_probe(blocks: int, iters: int, d_out, stream=None) -> float:
+    """Run the integer VALU throughput probe into the uint32/int32 device
+    tensor d_out (blocks * 256 words); returns its int32 lane operations."""
+    assert d_out.numel() >= blocks * 256 and d_out.element_size() == 4 and d_out.is_contiguous()
+    ops = ctypes.c_double()
+    _check(lib().sched_valu_probe(blocks, iters, d_out.data_ptr(), _stream_ptr(stream),
+                                  ctypes.byref(ops)), "sched_valu_probe")
+    return ops.value
 
 
 def sched_eval_reprobes(handle, base_index: int, workspace, lat=None,

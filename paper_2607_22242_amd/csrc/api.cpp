@@ -1063,6 +1063,18 @@ int sched_pruned_argmin(const sched_problem* p, void* d_workspace, size_t ws_byt
   return SCHED_OK;
 }
 
+int sched_valu_probe(uint32_t blocks, uint32_t iters, uint32_t* d_out, void* hip_stream,
+                     double* lane_ops) {
+  if (d_out == nullptr || lane_ops == nullptr) return SCHED_E_NULL;
+  if (blocks == 0 || iters == 0 || blocks > (1u << 24)) return SCHED_E_SIZE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  double ops = 0;
+  HIP_TRY(launch_valu_probe(blocks, iters, d_out, s, &ops));
+  HIP_TRY(hipStreamSynchronize(s));
+  *lane_ops = ops;
+  return SCHED_OK;
+}
+
 const char* sched_strerror(int code) {
   switch (code) {
     case SCHED_OK: return "ok";

@@ -13,5 +13,7 @@ hipError_t launch_bound(int n_tools, const uint32_t* tab, uint32_t K, uint64_t k
                         uint32_t ub, uint32_t* count, uint2* out, hipStream_t s);
 hipError_t launch_reduce(const Partial* partials, uint32_t per_table, uint32_t n_tables,
                          DevResult* out, hipStream_t s);
+hipError_t launch_valu_probe(uint32_t blocks, uint32_t iters, uint32_t* out, hipStream_t s,
+                             double* lane_ops);
 
 }  // namespace devmap

@@ -179,3 +179,16 @@ def test_strerror_covers_codes():
     for code, name in B.ERRORS.items():
         assert S.sched_strerror(code) != "unknown error", name
     assert S.sched_strerror(0) == "ok"
+
+
+def test_valu_probe_argument_validation():
+    """Argument errors come back before any device work."""
+    L = B.lib()
+    ops = ctypes.c_double()
+    dummy = ctypes.c_void_p(256)
+    assert B.ERRORS[L.sched_valu_probe(1, 1, None, None, ctypes.byref(ops))] == "SCHED_E_NULL"
+    assert B.ERRORS[L.sched_valu_probe(1, 1, dummy, None, None)] == "SCHED_E_NULL"
+    assert B.ERRORS[L.sched_valu_probe(0, 1, dummy, None, ctypes.byref(ops))] == "SCHED_E_SIZE"
+    assert B.ERRORS[L.sched_valu_probe(1, 0, dummy, None, ctypes.byref(ops))] == "SCHED_E_SIZE"
+    assert B.ERRORS[L.sched_valu_probe((1 << 24) + 1, 1, dummy, None,
+                                       ctypes.byref(ops))] == "SCHED_E_SIZE"
