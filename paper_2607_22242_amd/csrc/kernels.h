@@ -607,11 +607,15 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
 }
 
 // Waves per SIMD the search kernel is compiled for (the register budget):
-// 8 up to 16 tools, 6 beyond (measured: 6 waves take the 19-tool search from
-// 114 to 102 ms and the 32-tool one from 459 to 264 ms; the 14-tool batch
-// runs 10 % faster at 8).
+// 8 up to 16 tools, 7 up to 19 (the shared-prefix LDS column of N words per
+// lane then allows 7 blocks per CU, and the state fits 72 registers), 6
+// beyond.  Measured on the 19-tool search: 7 waves 58.4 ms against 6 waves
+// 64.2 ms; on the 32-tool one 6 waves took 264 ms against 459 ms at 8.
 #ifndef DEVMAP_SEARCH_WAVES_SMALL
 #define DEVMAP_SEARCH_WAVES_SMALL 8
+#endif
+#ifndef DEVMAP_SEARCH_WAVES_MID
+#define DEVMAP_SEARCH_WAVES_MID 7
 #endif
 #ifndef DEVMAP_SEARCH_WAVES_LARGE
 #define DEVMAP_SEARCH_WAVES_LARGE 6
@@ -739,28 +743,29 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // reuses after it, where other lanes are active.
 template <int N>
 constexpr uint32_t snap_words() {
-  // T of every tool, t, qfin, minq, mk (the masks stay in registers)
-  return N <= kPrefixMaxN ? uint32_t(N) + 4u : 1u;
+  // T of every tool (the masks and times stay in registers)
+  return N <= kPrefixMaxN ? uint32_t(N) : 1u;
 }
 
-// A lane's saved schedule state: the words in its LDS column s, the masks in
+// A lane's saved schedule state: T in its LDS column s, the rest in
 // registers.
 template <int N>
 struct Snap {
   MaskT<N> started, resolved, run;
+  uint32_t t, qfin, minq, mk;
 };
 
 template <int N>
 __host__ __device__ __forceinline__ void snap_save(uint32_t* s, Snap<N>& m, const Sim<N>& sim) {
 #pragma unroll
   for (int i = 0; i < N; ++i) s[i * kBlock] = sim.T[i];
-  s[(N + 0) * kBlock] = sim.t;
-  s[(N + 1) * kBlock] = sim.qfin;
-  s[(N + 2) * kBlock] = sim.minq;
-  s[(N + 3) * kBlock] = sim.mk;
   m.started = sim.started;
   m.resolved = sim.resolved;
   m.run = sim.run;
+  m.t = sim.t;
+  m.qfin = sim.qfin;
+  m.minq = sim.minq;
+  m.mk = sim.mk;
 }
 
 template <int N>
@@ -768,13 +773,13 @@ __host__ __device__ __forceinline__ void snap_load(const uint32_t* s, const Snap
                                                    Sim<N>& sim) {
 #pragma unroll
   for (int i = 0; i < N; ++i) sim.T[i] = s[i * kBlock];
-  sim.t = s[(N + 0) * kBlock];
-  sim.qfin = s[(N + 1) * kBlock];
-  sim.minq = s[(N + 2) * kBlock];
-  sim.mk = s[(N + 3) * kBlock];
   sim.started = m.started;
   sim.resolved = m.resolved;
   sim.run = m.run;
+  sim.t = m.t;
+  sim.qfin = m.qfin;
+  sim.minq = m.minq;
+  sim.mk = m.mk;
 }
 
 // lane_search for a full range with shared prefixes (see above); the inner
@@ -884,7 +889,8 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
 template <int N, bool FULL, bool SHARE>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
     SHARE ? DEVMAP_SHARE_WAVES
-          : (N <= 16 ? DEVMAP_SEARCH_WAVES_SMALL : DEVMAP_SEARCH_WAVES_LARGE)))) void
+          : (N <= 16 ? DEVMAP_SEARCH_WAVES_SMALL
+                     : (N <= 19 ? DEVMAP_SEARCH_WAVES_MID : DEVMAP_SEARCH_WAVES_LARGE))))) void
 search_kernel(SearchArgs a) {
   __shared__ uint32_t s_lds[lds_words<N>()];
   __shared__ uint64_t s_wave_words[kBlock / 64];  // one 8-byte word per wave
