@@ -211,6 +211,11 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
   return SCHED_OK;
 }
 
+// Contention levels stored in a problem's table.
+uint32_t table_levels(const sched_problem& p) {
+  return uint32_t(std::min<int>(int(p.contention.size()), p.n));
+}
+
 // Enumeration order (tools, inner positions first) of a search with J inner
 // digits.  Index order (a partial range): the tools with a choice in
 // ascending number, so that the walk follows the index.  A full range: the
@@ -300,6 +305,7 @@ void plan_search(const sched_problem& p, uint64_t lo, uint64_t hi, uint32_t n_ta
   a.full_range = full ? 1u : 0u;
   a.sharing = uint32_t(p.sharing);
   a.prefix = prefix ? 1u : 0u;
+  a.lds_levels = table_levels(p);
 }
 
 // Write the enumeration order seq into a table built by build_table.
@@ -741,6 +747,8 @@ int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
     Group g{first, last, SearchArgs{}};
     const sched_problem& p0 = *problems[pf];
     plan_search(p0, 0, p0.n_mappings, uint32_t(last - first), g.a);
+    for (size_t i = first; i < last; ++i)
+      g.a.lds_levels = std::max(g.a.lds_levels, table_levels(*problems[replica_problem[order[i]]]));
     // The block cap is shared by the whole batch so partials stay bounded.
     const uint64_t cap = std::max<uint64_t>(1, kMaxBlocks / R);
     g.a.blocks_per_table = uint32_t(std::min<uint64_t>(g.a.items_per_table, cap));

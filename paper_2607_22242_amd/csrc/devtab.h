@@ -121,6 +121,7 @@ struct SearchArgs {
   uint32_t sharing;           // 1: processor-sharing contention
   uint32_t prefix;            // 1: shared prefixes (kSharedInner inner digits on the
                               //    deepest tools, full range, fixed at start)
+  uint32_t lds_levels;        // the most contention levels any of the tables stores
 };
 
 struct DevResult {

@@ -96,16 +96,24 @@ __host__ __device__ __forceinline__ bool bit(MaskT<N> m, int v) {
   return (m >> v) & 1;
 }
 
-// LDS image staged by every block: the duration table, then footprints by
-// internal label, then the internal label of every original tool.
+// LDS image staged by every block: footprints by internal label, then the
+// internal label of every original tool, then the duration table (its
+// length follows the problem's contention levels).
 template <int N>
 constexpr uint32_t lds_levels() { return N < kMaxLevels ? N : kMaxLevels; }
 template <int N>
-constexpr uint32_t lds_mem_off() { return uint32_t(N) * 2u * lds_levels<N>(); }
+constexpr uint32_t lds_mem_off() { return 0u; }
 template <int N>
-constexpr uint32_t lds_pos_off() { return lds_mem_off<N>() + uint32_t(N); }
+constexpr uint32_t lds_pos_off() { return uint32_t(N); }
 template <int N>
-constexpr uint32_t lds_words() { return lds_pos_off<N>() + uint32_t(N); }
+constexpr uint32_t lds_dur_off() { return 2u * uint32_t(N); }
+// Words of the image for `levels` stored contention levels.
+__host__ __device__ constexpr uint32_t lds_words_for(int n, uint32_t levels) {
+  return 2u * uint32_t(n) + uint32_t(n) * 2u * levels;
+}
+// The largest image a problem with N tools can need.
+template <int N>
+constexpr uint32_t lds_words() { return lds_words_for(N, lds_levels<N>()); }
 
 // Bitwise OR of x over the active lanes of the calling wave, through one LDS
 // word per wave (slot).  Lanes that have left the calling loop simply do not
@@ -248,7 +256,7 @@ struct Sim {
     if (dead) return true;
     const M ALL = all_tools<N>();
     const M gpum = gnm | gqm;
-    const uint32_t* s_dur = lds;
+    const uint32_t* s_dur = lds + lds_dur_off<N>();
     const uint32_t* s_mem = lds + lds_mem_off<N>();
     const uint32_t* s_pos = lds + lds_pos_off<N>();
     const Tab tp = fresh(tab);
@@ -571,7 +579,8 @@ template <int N>
 __device__ __forceinline__ void stage_tables(const uint32_t* tab, uint32_t* lds) {
   const uint32_t levels = tab[kHdrLevels];
   const uint32_t* dur = tab + tab[kHdrDurOff];
-  for (uint32_t i = threadIdx.x; i < uint32_t(N) * 2u * levels; i += blockDim.x) lds[i] = dur[i];
+  for (uint32_t i = threadIdx.x; i < uint32_t(N) * 2u * levels; i += blockDim.x)
+    lds[lds_dur_off<N>() + i] = dur[i];
   for (uint32_t i = threadIdx.x; i < uint32_t(N); i += blockDim.x) {
     lds[lds_mem_off<N>() + i] = tab[kHdrWords + kToolWords * i + kToolMem];
     lds[lds_pos_off<N>() + i] = tab[kPosBase + i];
@@ -607,15 +616,15 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
 }
 
 // Waves per SIMD the search kernel is compiled for (the register budget):
-// 8 up to 16 tools, 7 up to 19 (the shared-prefix LDS column of N words per
-// lane then allows 7 blocks per CU, and the state fits 72 registers), 6
-// beyond.  Measured on the 19-tool search: 7 waves 58.4 ms against 6 waves
-// 64.2 ms; on the 32-tool one 6 waves took 264 ms against 459 ms at 8.
+// 8 up to 19 tools, 6 beyond.  Up to 19 tools the shared-prefix LDS column
+// (N words per lane) and the staged tables (sized by the problem's levels)
+// let 8 blocks share a CU, and 8 waves pay for their few spilled registers.
+// Measured: 19 tools 53.9 ms at 8 waves, 58.7 at 7, 64.2 at 6; random 17-
+// and 18-tool DAGs 7.9 / 18.3 ms at 8 against 8.6 / 19.5 at 7.  From 20
+// tools on, 64-bit indices take more registers; the 32-tool search ran 264
+// ms at 6 waves against 459 at 8.
 #ifndef DEVMAP_SEARCH_WAVES_SMALL
 #define DEVMAP_SEARCH_WAVES_SMALL 8
-#endif
-#ifndef DEVMAP_SEARCH_WAVES_MID
-#define DEVMAP_SEARCH_WAVES_MID 7
 #endif
 #ifndef DEVMAP_SEARCH_WAVES_LARGE
 #define DEVMAP_SEARCH_WAVES_LARGE 6
@@ -889,10 +898,10 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
 template <int N, bool FULL, bool SHARE>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
     SHARE ? DEVMAP_SHARE_WAVES
-          : (N <= 16 ? DEVMAP_SEARCH_WAVES_SMALL
-                     : (N <= 19 ? DEVMAP_SEARCH_WAVES_MID : DEVMAP_SEARCH_WAVES_LARGE))))) void
+          : (N <= 19 ? DEVMAP_SEARCH_WAVES_SMALL : DEVMAP_SEARCH_WAVES_LARGE)))) void
 search_kernel(SearchArgs a) {
-  __shared__ uint32_t s_lds[lds_words<N>()];
+  // the staged tables: lds_words_for(N, a.lds_levels) words, sized at launch
+  extern __shared__ uint32_t s_lds[];
   __shared__ uint64_t s_wave_words[kBlock / 64];  // one 8-byte word per wave
   MaskT<N>* const slot = reinterpret_cast<MaskT<N>*>(&s_wave_words[threadIdx.x / 64]);
   constexpr bool kPrefix = FULL && !SHARE && N <= kPrefixMaxN;
@@ -1030,16 +1039,18 @@ __global__ __launch_bounds__(kBlock) void bound_kernel(const uint32_t* __restric
 template <int N>
 hipError_t launch_search_n(const SearchArgs& a, hipStream_t s) {
   const uint32_t blocks = a.n_tables * a.blocks_per_table;
+  if (a.lds_levels < 1 || a.lds_levels > lds_levels<N>()) return hipErrorInvalidValue;
+  const size_t shm = size_t(lds_words_for(N, a.lds_levels)) * 4u;
   if (a.sharing) {
     if (a.full_range)
-      hipLaunchKernelGGL((search_kernel<N, true, true>), dim3(blocks), dim3(kBlock), 0, s, a);
+      hipLaunchKernelGGL((search_kernel<N, true, true>), dim3(blocks), dim3(kBlock), shm, s, a);
     else
-      hipLaunchKernelGGL((search_kernel<N, false, true>), dim3(blocks), dim3(kBlock), 0, s, a);
+      hipLaunchKernelGGL((search_kernel<N, false, true>), dim3(blocks), dim3(kBlock), shm, s, a);
   } else {
     if (a.full_range)
-      hipLaunchKernelGGL((search_kernel<N, true, false>), dim3(blocks), dim3(kBlock), 0, s, a);
+      hipLaunchKernelGGL((search_kernel<N, true, false>), dim3(blocks), dim3(kBlock), shm, s, a);
     else
-      hipLaunchKernelGGL((search_kernel<N, false, false>), dim3(blocks), dim3(kBlock), 0, s, a);
+      hipLaunchKernelGGL((search_kernel<N, false, false>), dim3(blocks), dim3(kBlock), shm, s, a);
   }
   return hipGetLastError();
 }
