@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 15247360
-TRAFFIC_KERNEL_SHA256 = "5c86fd2b00014d3f8cfb513f28851ed9be92c937e8947e4b8fd579e9abd8eafe"
+TRAFFIC_BYTES = 65369216
+TRAFFIC_KERNEL_SHA256 = "df0ce53abf461ae0928af6d7ef44d9f0ae293c1bb79838d7e7aad936f8ace90d"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 
