@@ -420,6 +420,21 @@ __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict
   return ms;
 }
 
+// ceil(a / w) for a < 2^53 and 1 <= w < 2^17, exactly: a double estimate of
+// the quotient (off by at most one) corrected with integer remainders.
+__host__ __device__ __forceinline__ uint64_t ceil_div_small(uint64_t a, uint32_t w) {
+  uint64_t q = uint64_t(double(a) / double(w));
+  int64_t r = int64_t(a) - int64_t(q * uint64_t(w));
+  if (r < 0) {
+    q -= 1;
+    r += int64_t(w);
+  } else if (r >= int64_t(w)) {
+    q += 1;
+    r -= int64_t(w);
+  }
+  return q + (r > 0 ? 1u : 0u);
+}
+
 // Makespan under processor sharing, or kInf if infeasible.  The events are
 // those of the fixed-at-start schedule (release, immediate starts with the
 // VRAM check, one queue admission in (ready, tool) order), but a GPU task's
@@ -427,17 +442,22 @@ __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict
 // rate w_k of the k GPU tasks running, so with V the work each has done
 // since time 0, a task started at V_s with work b * 2^16 ends when V reaches
 // its virtual finish V_s + b * 2^16.  Per lane: X[i] holds the ready time of
-// a waiting task and the end of a started one.
+// a waiting task and the end of a started one.  Each per-tool loop visits a
+// tool only where some lane of the wave has it running or waiting (two
+// wave-wide ORs per pass); elsewhere the tool is done everywhere and its
+// work would change nothing.
 template <int N>
 __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __restrict__ tab,
                                                               const uint32_t* __restrict__ lds,
                                                               uint32_t levels, uint32_t budget,
-                                                              MaskT<N> gnm, MaskT<N> gqm) {
+                                                              MaskT<N> gnm, MaskT<N> gqm,
+                                                              MaskT<N>* slot) {
   using M = MaskT<N>;
   const Tab tp{tab};
   const uint32_t* s_mem = lds + lds_mem_off<N>();
   const uint32_t* sh = tab + tab[kHdrShareOff];
   const M gpu = gnm | gqm;
+  const M ALL = all_tools<N>();
   if ((gpu & load_mask<N>(tp, kHdrBigLo)) != 0) return kInf;
   uint32_t X[N];
   uint64_t VF[N];
@@ -450,11 +470,26 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
     VF[i] = 0;
   }
   for (int pass = 0; pass < 4 * N + 4; ++pass) {
+    // tools some lane of the wave has running / waiting
+    M wr, ww;
+    if constexpr (N <= 32) {
+      const uint64_t both = wave_or<uint64_t>(
+          uint64_t(running) | (uint64_t(ALL & ~(running | done)) << 32),
+          reinterpret_cast<uint64_t*>(slot));
+      wr = M(both);
+      ww = M(both >> 32);
+    } else {
+      wr = wave_or<M>(running, slot);
+      ww = wave_or<M>(ALL & ~(running | done), slot);
+    }
     // 1. release: CPU tasks at their end, GPU tasks out of work
+    const M wr1 = opaque(wr);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      if ((running >> i) & 1) {
-        const bool fin = ((gpu >> i) & 1) ? VF[i] <= V : X[i] <= t;
+      if ((wr1 >> i) & 1) {
+        DEVMAP_KEEP_BRANCH();
+        const bool fin = ((running >> i) & 1) &&
+                         (((gpu >> i) & 1) ? VF[i] <= V : X[i] <= t);
         if (fin) {
           running &= ~(M(1) << i);
           done |= M(1) << i;
@@ -462,20 +497,26 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
         }
       }
     }
-    if (done == all_tools<N>()) return t;
+    if (done == ALL) return t;
     // 2. ready times of waiting tasks whose predecessors are done, and the
     // immediate starts
-    const M waiting = ~(running | done) & all_tools<N>();
+    const M waiting = ~(running | done) & ALL;
     M ready = 0, starting = 0;
     uint32_t in_use = 0;
+    const M wr2 = opaque(wr);
 #pragma unroll
     for (int i = 0; i < N; ++i)
-      if ((running >> i) & 1 && (gpu >> i) & 1) in_use += s_mem[i];
+      if ((wr2 >> i) & 1) {
+        DEVMAP_KEEP_BRANCH();
+        if ((running >> i) & 1 && (gpu >> i) & 1) in_use += s_mem[i];
+      }
+    const M ww2 = opaque(ww);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      if ((waiting >> i) & 1) {
+      if ((ww2 >> i) & 1) {
+        DEVMAP_KEEP_BRANCH();
         const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
-        if ((pm & ~done) == 0) {
+        if ((waiting >> i) & 1 && (pm & ~done) == 0) {
           const uint32_t xf = tp[kHdrWords + kToolWords * i + kToolXfer];
           uint32_t r = 0;
 #pragma unroll
@@ -496,29 +537,35 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
     if ((running & gqm) == 0) {
       int head = -1;
       uint32_t hr = kInf, ho = kInf;
+      const M ww3 = opaque(ww);
 #pragma unroll
       for (int i = 0; i < N; ++i) {
-        if ((ready >> i) & 1 && (gqm >> i) & 1 && X[i] <= t) {
-          const uint32_t o = tp[kHdrWords + kToolWords * i + kToolOrig];
-          if (X[i] < hr || (X[i] == hr && o < ho)) {
-            head = i;
-            hr = X[i];
-            ho = o;
+        if ((ww3 >> i) & 1) {
+          DEVMAP_KEEP_BRANCH();
+          if ((ready >> i) & 1 && (gqm >> i) & 1 && X[i] <= t) {
+            const uint32_t o = tp[kHdrWords + kToolWords * i + kToolOrig];
+            if (X[i] < hr || (X[i] == hr && o < ho)) {
+              head = i;
+              hr = X[i];
+              ho = o;
+            }
           }
         }
       }
-#pragma unroll
-      for (int i = 0; i < N; ++i)
-        if (i == head && s_mem[i] <= budget - in_use) starting |= M(1) << i;
+      if (head >= 0 && s_mem[head] <= budget - in_use) starting |= M(1) << head;
     }
     // 4. starts
+    const M ww4 = opaque(ww);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      if ((starting >> i) & 1) {
-        if ((gpu >> i) & 1)
-          VF[i] = V + (uint64_t(sh[2 * i + (((gqm >> i) & 1) ? 1 : 0)]) << 16);
-        else
-          X[i] = t + tp[kHdrWords + kToolWords * i + kToolCpu];
+      if ((ww4 >> i) & 1) {
+        DEVMAP_KEEP_BRANCH();
+        if ((starting >> i) & 1) {
+          if ((gpu >> i) & 1)
+            VF[i] = V + (uint64_t(sh[2 * i + (((gqm >> i) & 1) ? 1 : 0)]) << 16);
+          else
+            X[i] = t + tp[kHdrWords + kToolWords * i + kToolCpu];
+        }
       }
     }
     running |= starting;
@@ -526,19 +573,23 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
     const M rg = running & gpu;
     uint32_t next = kInf, k = 0;
     uint64_t vmin = ~0ull;
+    const M wa5 = opaque(wr | ww);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      if ((rg >> i) & 1) {
-        ++k;
-        vmin = vmin < VF[i] ? vmin : VF[i];
+      if ((wa5 >> i) & 1) {
+        DEVMAP_KEEP_BRANCH();
+        if ((rg >> i) & 1) {
+          ++k;
+          vmin = vmin < VF[i] ? vmin : VF[i];
+        }
+        if ((running >> i) & 1 && !((gpu >> i) & 1)) next = umin32(next, X[i]);
+        if ((ready >> i) & 1 && !((starting >> i) & 1) && X[i] > t) next = umin32(next, X[i]);
       }
-      if ((running >> i) & 1 && !((gpu >> i) & 1)) next = umin32(next, X[i]);
-      if ((ready >> i) & 1 && !((starting >> i) & 1) && X[i] > t) next = umin32(next, X[i]);
     }
-    uint64_t w = 0;
+    uint32_t w = 0;
     if (k) {
       w = sh[2 * N + (k < levels ? k : levels) - 1];
-      next = umin32(next, t + uint32_t((vmin - V + w - 1) / w));
+      next = umin32(next, t + uint32_t(ceil_div_small(vmin - V, w)));
     }
     if (next == kInf) return kInf;  // a queued task never fits
     V += uint64_t(next - t) * w;
@@ -630,9 +681,10 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
 #define DEVMAP_SEARCH_WAVES_LARGE 6
 #endif
 // The same for the processor-sharing evaluator, which keeps a 64-bit virtual
-// finish per tool.
+// finish per tool: 4 waves, some registers spilled (19 tools: 638 ms at 4
+// waves, 717 at 3, 995 at 2 without spills).
 #ifndef DEVMAP_SHARE_WAVES
-#define DEVMAP_SHARE_WAVES 2
+#define DEVMAP_SHARE_WAVES 4
 #endif
 
 // Index arithmetic: 3^20 < 2^32, so up to 20 tools an index fits 32 bits.
@@ -692,7 +744,7 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
     if (FULL || (i >= ilo && i < ihi)) {
       uint32_t ms;
       if constexpr (SHARE)
-        ms = evaluate_sharing<N>(tab, lds, levels, budget, ogn | ign, ogq | igq);
+        ms = evaluate_sharing<N>(tab, lds, levels, budget, ogn | ign, ogq | igq, slot);
       else
         ms = evaluate<N>(tab, lds, levels, budget, ogn | ign, ogq | igq, slot);
       if constexpr (FULL) {
@@ -962,7 +1014,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(const uint32_t* __restrict
       decode_positions<N>(tab, x, 0, tab[kHdrPositions], gn, gq, xw);
       uint32_t ms;
       if constexpr (SHARE)
-        ms = evaluate_sharing<N>(tab, s_lds, levels, budget, gn, gq);
+        ms = evaluate_sharing<N>(tab, s_lds, levels, budget, gn, gq, slot);
       else
         ms = evaluate<N>(tab, s_lds, levels, budget, gn, gq, slot);
       if (ms != kInf) r = int64_t(ms);

@@ -176,6 +176,32 @@ def test_batch_matches_oracle_small_mixed_sizes(torch_cuda, O):
         assert got[r] == Q.argmin(threads=1), r
 
 
+@pytest.mark.parametrize("n,levels", [(14, 14), (14, 1), (14, 2)])
+def test_full_search_contention_levels(torch_cuda, O, n, levels):
+    """The staged duration table is sized by the problem's levels: one level,
+    two, and as many as tools, on the shared-prefix path (full range)."""
+    inst = synth.random_instance(6100 + n * 7 + levels, n, "random", levels=levels,
+                                 tight=levels != 1)
+    P, Q = both(inst, O)
+    say(f"full search n={n} levels={levels}")
+    assert gpu_argmin(torch_cuda, P) == Q.argmin()
+
+
+def test_batch_groups_with_different_levels(torch_cuda, O):
+    """Replicas of one plan whose problems store different numbers of
+    contention levels share a launch; its LDS is sized for the most."""
+    insts = [synth.random_instance(6200 + i, 13, "random", levels=lv, tight=True)
+             for i, lv in enumerate([1, 13, 4])]
+    problems = [S.Problem.from_instance(i) for i in insts]
+    rp = [0, 1, 2, 1, 0, 2]
+    lat = [synth.perturb(insts[p]["tools"], 6300 + r) for r, p in enumerate(rp)]
+    ws = S.workspace([p.handle for p in problems], len(rp))
+    say("eval_batch, levels 1 / 13 / 4 in one group")
+    got = S.sched_eval_batch([p.handle for p in problems], rp, lat, ws)
+    for r in range(len(rp)):
+        assert got[r] == O.Problem.from_instance(insts[rp[r]], lat[r]).argmin(), r
+
+
 @pytest.mark.parametrize("c", [1, 2])
 def test_ragged_ranges(torch_cuda, O, c):
     P, Q = both(synth.load(c), O)
