@@ -441,8 +441,7 @@ __host__ __device__ __forceinline__ uint64_t ceil_div_small(uint64_t a, uint32_t
 // end is not fixed when it starts: every running GPU task advances at the
 // rate w_k of the k GPU tasks running, so with V the work each has done
 // since time 0, a task started at V_s with work b * 2^16 ends when V reaches
-// its virtual finish V_s + b * 2^16.  Per lane: X[i] holds the ready time of
-// a waiting task and the end of a started one.  Each per-tool loop visits a
+// its virtual finish V_s + b * 2^16.  Each per-tool loop visits a
 // tool only where some lane of the wave has it running or waiting (two
 // wave-wide ORs per pass); elsewhere the tool is done everywhere and its
 // work would change nothing.
@@ -459,16 +458,14 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
   const M gpu = gnm | gqm;
   const M ALL = all_tools<N>();
   if ((gpu & load_mask<N>(tp, kHdrBigLo)) != 0) return kInf;
-  uint32_t X[N];
-  uint64_t VF[N];
+  // Y[i]: the virtual finish of a running GPU task, else (low word) its
+  // ready time while waiting and its end once started or done
+  uint64_t Y[N];
   M running = 0, done = 0;
   uint64_t V = 0;
   uint32_t t = 0;
 #pragma unroll
-  for (int i = 0; i < N; ++i) {
-    X[i] = 0;
-    VF[i] = 0;
-  }
+  for (int i = 0; i < N; ++i) Y[i] = 0;
   for (int pass = 0; pass < 4 * N + 4; ++pass) {
     // tools some lane of the wave has running / waiting
     M wr, ww;
@@ -489,11 +486,11 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
       if ((wr1 >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
         const bool fin = ((running >> i) & 1) &&
-                         (((gpu >> i) & 1) ? VF[i] <= V : X[i] <= t);
+                         (((gpu >> i) & 1) ? Y[i] <= V : uint32_t(Y[i]) <= t);
         if (fin) {
           running &= ~(M(1) << i);
           done |= M(1) << i;
-          X[i] = t;
+          Y[i] = t;
         }
       }
     }
@@ -522,8 +519,8 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
 #pragma unroll
           for (int u = 0; u < i; ++u)
             if ((pm >> u) & 1)
-              r = umax32(r, X[u] + ((((gpu >> u) ^ (gpu >> i)) & 1) ? xf : 0u));
-          X[i] = r;
+              r = umax32(r, uint32_t(Y[u]) + ((((gpu >> u) ^ (gpu >> i)) & 1) ? xf : 0u));
+          Y[i] = r;
           ready |= M(1) << i;
           if (r <= t && !((gqm >> i) & 1)) {
             starting |= M(1) << i;
@@ -542,11 +539,12 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
       for (int i = 0; i < N; ++i) {
         if ((ww3 >> i) & 1) {
           DEVMAP_KEEP_BRANCH();
-          if ((ready >> i) & 1 && (gqm >> i) & 1 && X[i] <= t) {
+          const uint32_t x = uint32_t(Y[i]);
+          if ((ready >> i) & 1 && (gqm >> i) & 1 && x <= t) {
             const uint32_t o = tp[kHdrWords + kToolWords * i + kToolOrig];
-            if (X[i] < hr || (X[i] == hr && o < ho)) {
+            if (x < hr || (x == hr && o < ho)) {
               head = i;
-              hr = X[i];
+              hr = x;
               ho = o;
             }
           }
@@ -562,9 +560,9 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
         DEVMAP_KEEP_BRANCH();
         if ((starting >> i) & 1) {
           if ((gpu >> i) & 1)
-            VF[i] = V + (uint64_t(sh[2 * i + (((gqm >> i) & 1) ? 1 : 0)]) << 16);
+            Y[i] = V + (uint64_t(sh[2 * i + (((gqm >> i) & 1) ? 1 : 0)]) << 16);
           else
-            X[i] = t + tp[kHdrWords + kToolWords * i + kToolCpu];
+            Y[i] = t + tp[kHdrWords + kToolWords * i + kToolCpu];
         }
       }
     }
@@ -580,10 +578,11 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
         DEVMAP_KEEP_BRANCH();
         if ((rg >> i) & 1) {
           ++k;
-          vmin = vmin < VF[i] ? vmin : VF[i];
+          vmin = vmin < Y[i] ? vmin : Y[i];
         }
-        if ((running >> i) & 1 && !((gpu >> i) & 1)) next = umin32(next, X[i]);
-        if ((ready >> i) & 1 && !((starting >> i) & 1) && X[i] > t) next = umin32(next, X[i]);
+        const uint32_t x = uint32_t(Y[i]);
+        if ((running >> i) & 1 && !((gpu >> i) & 1)) next = umin32(next, x);
+        if ((ready >> i) & 1 && !((starting >> i) & 1) && x > t) next = umin32(next, x);
       }
     }
     uint32_t w = 0;
@@ -681,10 +680,10 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
 #define DEVMAP_SEARCH_WAVES_LARGE 6
 #endif
 // The same for the processor-sharing evaluator, which keeps a 64-bit virtual
-// finish per tool: 4 waves, some registers spilled (19 tools: 638 ms at 4
-// waves, 717 at 3, 995 at 2 without spills).
+// finish per tool: 5 waves, some registers spilled (19 tools: 549 ms at 5
+// waves, 594 at 4, 721 at 6; 8 waves do not fit).
 #ifndef DEVMAP_SHARE_WAVES
-#define DEVMAP_SHARE_WAVES 4
+#define DEVMAP_SHARE_WAVES 5
 #endif
 
 // Index arithmetic: 3^20 < 2^32, so up to 20 tools an index fits 32 bits.
