@@ -435,38 +435,57 @@ __host__ __device__ __forceinline__ uint64_t ceil_div_small(uint64_t a, uint32_t
   return q + (r > 0 ? 1u : 0u);
 }
 
-// Makespan under processor sharing, or kInf if infeasible.  The events are
-// those of the fixed-at-start schedule (release, immediate starts with the
-// VRAM check, one queue admission in (ready, tool) order), but a GPU task's
-// end is not fixed when it starts: every running GPU task advances at the
-// rate w_k of the k GPU tasks running, so with V the work each has done
-// since time 0, a task started at V_s with work b * 2^16 ends when V reaches
-// its virtual finish V_s + b * 2^16.  Each per-tool loop visits a
-// tool only where some lane of the wave has it running or waiting (two
-// wave-wide ORs per pass); elsewhere the tool is done everywhere and its
-// work would change nothing.
+// Event loop under processor sharing, one event time per call of step().
+// The events are those of the fixed-at-start schedule (release, immediate
+// starts with the VRAM check, one queue admission in (ready, tool) order),
+// but a GPU task's end is not fixed when it starts: every running GPU task
+// advances at the rate w_k of the k GPU tasks running, so with V the work
+// each has done since time 0, a task started at V_s with work b * 2^16 ends
+// when V reaches its virtual finish V_s + b * 2^16.  Each per-tool loop
+// visits a tool only where some lane of the wave has it running or waiting
+// (two wave-wide ORs per pass); elsewhere the tool is done everywhere and
+// its work would change nothing.  A tool's mode is first read in the pass
+// that finds all its predecessors done (readym).
 template <int N>
-__host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __restrict__ tab,
-                                                              const uint32_t* __restrict__ lds,
-                                                              uint32_t levels, uint32_t budget,
-                                                              MaskT<N> gnm, MaskT<N> gqm,
-                                                              MaskT<N>* slot) {
+struct SimPS {
   using M = MaskT<N>;
-  const Tab tp{tab};
-  const uint32_t* s_mem = lds + lds_mem_off<N>();
-  const uint32_t* sh = tab + tab[kHdrShareOff];
-  const M gpu = gnm | gqm;
-  const M ALL = all_tools<N>();
-  if ((gpu & load_mask<N>(tp, kHdrBigLo)) != 0) return kInf;
   // Y[i]: the virtual finish of a running GPU task, else (low word) its
   // ready time while waiting and its end once started or done
   uint64_t Y[N];
-  M running = 0, done = 0;
-  uint64_t V = 0;
-  uint32_t t = 0;
+  M gnm, gqm;
+  M running, done;
+  M readym;  // tools whose predecessors were all done at the last pass
+  uint64_t V;
+  uint32_t t;
+  bool dead;  // statically infeasible
+
+  __host__ __device__ __forceinline__ void init(const uint32_t* __restrict__ tab, M gn, M gq) {
+    gnm = gn;
+    gqm = gq;
 #pragma unroll
-  for (int i = 0; i < N; ++i) Y[i] = 0;
-  for (int pass = 0; pass < 4 * N + 4; ++pass) {
+    for (int i = 0; i < N; ++i) Y[i] = 0;
+    running = 0;
+    done = 0;
+    readym = 0;
+    V = 0;
+    t = 0;
+    dead = ((gn | gq) & load_mask<N>(Tab{tab}, kHdrBigLo)) != 0;
+  }
+
+  // One event time.  Returns true when the mapping is settled; ms then holds
+  // its makespan, or kInf if it is infeasible.
+  __host__ __device__ __forceinline__ bool step(const uint32_t* __restrict__ tab,
+                                                const uint32_t* __restrict__ lds,
+                                                uint32_t levels, uint32_t budget, int pass,
+                                                M* slot, uint32_t& ms) {
+    (void)pass;
+    ms = kInf;
+    if (dead) return true;
+    const Tab tp{tab};
+    const uint32_t* s_mem = lds + lds_mem_off<N>();
+    const uint32_t* sh = tab + tab[kHdrShareOff];
+    const M gpu = gnm | gqm;
+    const M ALL = all_tools<N>();
     // tools some lane of the wave has running / waiting
     M wr, ww;
     if constexpr (N <= 32) {
@@ -494,7 +513,10 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
         }
       }
     }
-    if (done == ALL) return t;
+    if (done == ALL) {
+      ms = t;
+      return true;
+    }
     // 2. ready times of waiting tasks whose predecessors are done, and the
     // immediate starts
     const M waiting = ~(running | done) & ALL;
@@ -529,7 +551,7 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
         }
       }
     }
-    if (in_use > budget) return kInf;
+    if (in_use > budget) return true;  // out of memory: infeasible
     // 3. one queue admission when no queued task runs: FIFO on (ready, tool)
     if ((running & gqm) == 0) {
       int head = -1;
@@ -567,6 +589,7 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
       }
     }
     running |= starting;
+    readym = ready;
     // 5. next event at the rate of the GPU tasks now running
     const M rg = running & gpu;
     uint32_t next = kInf, k = 0;
@@ -590,11 +613,27 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
       w = sh[2 * N + (k < levels ? k : levels) - 1];
       next = umin32(next, t + uint32_t(ceil_div_small(vmin - V, w)));
     }
-    if (next == kInf) return kInf;  // a queued task never fits
+    if (next == kInf) return true;  // a queued task never fits
     V += uint64_t(next - t) * w;
     t = next;
+    return false;
   }
-  return kInf;  // not reached: every pass starts, ends or readies a task
+};
+
+// Makespan under processor sharing, or kInf if infeasible (slot: the calling
+// wave's LDS word, see wave_or).
+template <int N>
+__host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __restrict__ tab,
+                                                              const uint32_t* __restrict__ lds,
+                                                              uint32_t levels, uint32_t budget,
+                                                              MaskT<N> gnm, MaskT<N> gqm,
+                                                              MaskT<N>* slot) {
+  SimPS<N> sim;
+  sim.init(tab, gnm, gqm);
+  uint32_t ms = kInf;
+  for (int pass = 0; pass < 4 * N + 4; ++pass)
+    if (sim.step(tab, lds, levels, budget, pass, slot, ms)) break;
+  return ms;
 }
 
 __device__ __forceinline__ void lex_min(uint32_t& ms, uint64_t& x, uint32_t oms, uint64_t ox) {
@@ -801,14 +840,14 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // 0): a branch per tool on the wave-uniform inner mask would be compiled as a
 // lane-mask test that the compiler computes inside the prefix loop and
 // reuses after it, where other lanes are active.
-template <int N>
+template <int N, bool SHARE>
 constexpr uint32_t snap_words() {
-  // T of every tool (the masks and times stay in registers)
-  return N <= kPrefixMaxN ? uint32_t(N) : 1u;
+  // the per-tool words of the state (the masks and times stay in registers)
+  return N <= kPrefixMaxN ? (SHARE ? 2u : 1u) * uint32_t(N) : 1u;
 }
 
-// A lane's saved schedule state: T in its LDS column s, the rest in
-// registers.
+// A lane's saved schedule state: the per-tool words in its LDS column s, the
+// rest in registers.
 template <int N>
 struct Snap {
   MaskT<N> started, resolved, run;
@@ -842,9 +881,57 @@ __host__ __device__ __forceinline__ void snap_load(const uint32_t* s, const Snap
   sim.mk = m.mk;
 }
 
-// lane_search for a full range with shared prefixes (see above); the inner
-// positions 0..kSharedInner-1 hold the deepest tools.
+// The tools whose mode the last pass read for the first time.
 template <int N>
+__host__ __device__ __forceinline__ MaskT<N> first_read(const Sim<N>& sim) {
+  return sim.resolved;
+}
+
+// The same for the processor-sharing evaluator: Y (two words per tool) in
+// LDS.
+template <int N>
+struct SnapPS {
+  MaskT<N> running, done;
+  uint64_t V;
+  uint32_t t;
+};
+
+template <int N>
+__host__ __device__ __forceinline__ void snap_save(uint32_t* s, SnapPS<N>& m,
+                                                   const SimPS<N>& sim) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    s[(2 * i) * kBlock] = uint32_t(sim.Y[i]);
+    s[(2 * i + 1) * kBlock] = uint32_t(sim.Y[i] >> 32);
+  }
+  m.running = sim.running;
+  m.done = sim.done;
+  m.V = sim.V;
+  m.t = sim.t;
+}
+
+template <int N>
+__host__ __device__ __forceinline__ void snap_load(const uint32_t* s, const SnapPS<N>& m,
+                                                   SimPS<N>& sim) {
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    sim.Y[i] = uint64_t(s[(2 * i) * kBlock]) | (uint64_t(s[(2 * i + 1) * kBlock]) << 32);
+  sim.running = m.running;
+  sim.done = m.done;
+  sim.readym = 0;
+  sim.V = m.V;
+  sim.t = m.t;
+}
+
+template <int N>
+__host__ __device__ __forceinline__ MaskT<N> first_read(const SimPS<N>& sim) {
+  return sim.readym;
+}
+
+// lane_search for a full range with shared prefixes (see above); the inner
+// positions 0..kSharedInner-1 hold the deepest tools.  SHARE: the
+// processor-sharing evaluator, whose saved state holds Y instead of T.
+template <int N, bool SHARE>
 __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
                                                             const uint32_t* __restrict__ tab,
                                                             const uint32_t* __restrict__ lds,
@@ -868,18 +955,21 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
   for (uint32_t j = 0; j < J; ++j) inner |= M(1) << tu[kEnumLabBase + j];
   const M big = load_mask<N>(tu, kHdrBigLo);
 
+  using S = typename std::conditional<SHARE, SimPS<N>, Sim<N>>::type;
+  using SS = typename std::conditional<SHARE, SnapPS<N>, Snap<N>>::type;
+  constexpr int kPasses = SHARE ? 4 * N + 4 : 2 * N + 2;
   // The prefix: inner tools on the CPU (their modes are never read before
   // one of them is resolved).  pstar: the first pass that resolves one.
   int pstar = -1;
-  Snap<N> sm;
+  SS sm;
   {
-    Sim<N> sim;
+    S sim;
     sim.init(tab, ogn, ogq);
-    for (int pass = 0; pass < 2 * N + 2; ++pass) {
+    for (int pass = 0; pass < kPasses; ++pass) {
       snap_save<N>(snap, sm, sim);
       uint32_t ms;
       const bool fin = sim.step(tab, lds, levels, budget, pass, slot, ms);
-      if (sim.resolved & inner) {
+      if (first_read<N>(sim) & inner) {
         pstar = pass;
         break;
       }
@@ -901,13 +991,13 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
     if (m == 2u) igq |= b;
   }
   for (uint32_t i = 0; i < a.inner_count; ++i) {
-    Sim<N> sim;
+    S sim;
     snap_load<N>(snap, sm, sim);
     sim.gnm = ogn | ign;
     sim.gqm = ogq | igq;
     sim.dead = ((sim.gnm | sim.gqm) & big) != 0;
     uint32_t ms = kInf;
-    for (int pass = pstar; pass < 2 * N + 2; ++pass)
+    for (int pass = pstar; pass < kPasses; ++pass)
       if (sim.step(tab, lds, levels, budget, pass, slot, ms)) break;
     if (ms <= best_ms) {
       const I x = xo + xi;
@@ -948,15 +1038,16 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
 // block's minimum goes to partials[b].
 template <int N, bool FULL, bool SHARE>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
-    SHARE ? DEVMAP_SHARE_WAVES
+    SHARE ? (FULL && N <= kPrefixMaxN ? (N <= 19 ? 4 : 3)  // LDS: 2N words per lane
+                                      : DEVMAP_SHARE_WAVES)
           : (N <= 19 ? DEVMAP_SEARCH_WAVES_SMALL : DEVMAP_SEARCH_WAVES_LARGE)))) void
 search_kernel(SearchArgs a) {
   // the staged tables: lds_words_for(N, a.lds_levels) words, sized at launch
   extern __shared__ uint32_t s_lds[];
   __shared__ uint64_t s_wave_words[kBlock / 64];  // one 8-byte word per wave
   MaskT<N>* const slot = reinterpret_cast<MaskT<N>*>(&s_wave_words[threadIdx.x / 64]);
-  constexpr bool kPrefix = FULL && !SHARE && N <= kPrefixMaxN;
-  __shared__ uint32_t s_snap[kPrefix ? snap_words<N>() * kBlock : 1];
+  constexpr bool kPrefix = FULL && N <= kPrefixMaxN;
+  __shared__ uint32_t s_snap[kPrefix ? snap_words<N, SHARE>() * kBlock : 1];
   const uint32_t table = blockIdx.x / a.blocks_per_table;
   const uint32_t bb = blockIdx.x - table * a.blocks_per_table;
   const uint32_t* tab = a.tables + size_t(table) * a.table_stride;
@@ -967,7 +1058,7 @@ search_kernel(SearchArgs a) {
   if constexpr (kPrefix) {
     if (a.prefix) {
       for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-        lane_search_prefix<N>(a, tab, s_lds, item, threadIdx.x, slot,
+        lane_search_prefix<N, SHARE>(a, tab, s_lds, item, threadIdx.x, slot,
                               s_snap + threadIdx.x, best_ms, best_x);
     } else {
       for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
