@@ -202,6 +202,17 @@ def test_batch_groups_with_different_levels(torch_cuda, O):
         assert got[r] == O.Problem.from_instance(insts[rp[r]], lat[r]).argmin(), r
 
 
+@pytest.mark.parametrize("seed,tight", [(6400, True), (6401, False)])
+def test_sharing_full_search_shared_prefixes(torch_cuda, O, seed, tight):
+    """A 14-tool full search under processor sharing takes the shared-prefix
+    plan (3^14 / 9 outer combinations fill the GPU); against the oracle."""
+    inst = synth.random_instance(seed, 14, "random", tight=tight)
+    P = S.Problem.from_instance(inst, sharing=True)
+    Q = O.Problem.from_instance(inst, sharing=True)
+    say(f"sharing full search n=14 seed={seed}")
+    assert gpu_argmin(torch_cuda, P) == Q.argmin()
+
+
 @pytest.mark.parametrize("c", [1, 2])
 def test_ragged_ranges(torch_cuda, O, c):
     P, Q = both(synth.load(c), O)
