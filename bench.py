@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 65369216
-TRAFFIC_KERNEL_SHA256 = "df0ce53abf461ae0928af6d7ef44d9f0ae293c1bb79838d7e7aad936f8ace90d"
+TRAFFIC_BYTES = 65193600
+TRAFFIC_KERNEL_SHA256 = "0c6acf1cadeb2cb9345336e74069c59335c64fd74a8abbb1612a420175131364"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 
