@@ -1059,7 +1059,7 @@ search_kernel(SearchArgs a) {
     if (a.prefix) {
       for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
         lane_search_prefix<N, SHARE>(a, tab, s_lds, item, threadIdx.x, slot,
-                              s_snap + threadIdx.x, best_ms, best_x);
+                                     s_snap + threadIdx.x, best_ms, best_x);
     } else {
       for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
         lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x,
