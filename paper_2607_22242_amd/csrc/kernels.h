@@ -24,13 +24,6 @@ namespace devmap {
 template <int N>
 using MaskT = typename std::conditional<(N <= 32), uint32_t, uint64_t>::type;
 
-// A wave-uniform value (scalar register); the identity in a host build.
-#if defined(__HIP_DEVICE_COMPILE__)
-#define DEVMAP_UNIFORM(x) __builtin_amdgcn_readfirstlane(x)
-#else
-#define DEVMAP_UNIFORM(x) (x)
-#endif
-
 // Read-only view of a problem table.  On the device it reads through the
 // constant address space, so wave-uniform reads become scalar loads.
 struct Tab {
