@@ -219,6 +219,7 @@ struct Sim {
   uint32_t qfin;  // finish of the running queued tool (0: none)
   uint32_t minq;  // earliest ready time of a waiting queued tool (>= H: none)
   uint32_t mk;    // latest finish of the started tools
+  uint32_t rgs;   // deferred tools: earliest ready time on the GPU (kInf: none known)
   bool dead;      // statically infeasible
 
   __host__ __device__ __forceinline__ void init(const uint32_t* __restrict__ tab, M gn, M gq) {
@@ -233,6 +234,7 @@ struct Sim {
     qfin = 0;
     minq = kInf;
     mk = 0;
+    rgs = kInf;
     // a GPU mode whose footprint exceeds the budget never fits
     dead = ((gn | gq) & load_mask<N>(Tab{tab}, kHdrBigLo)) != 0;
   }
@@ -241,10 +243,22 @@ struct Sim {
   // mappings together).  Returns true when the mapping is settled; ms then
   // holds its makespan, or kInf if it is infeasible.  slot: this wave's LDS
   // word for the wave-wide masks.
+  //
+  // DEFER (schedule prefixes shared by the modes of `defer`, a wave-uniform
+  // set of sinks that have predecessors): a deferred tool's mode is never
+  // read.  When its predecessors have all started it is marked resolved and
+  // started with T = 0, which keeps it out of every later per-tool loop, and
+  // its ready time on the GPU joins rgs, which is an event.  Before that
+  // time the tool cannot run, hold VRAM, queue or feed a successor in any
+  // mode (and on the CPU it only adds its own finish to the makespan), so
+  // the passes before rgs are those of every mode.  Once a deferred tool is
+  // resolved a pass ends the mapping only as infeasible; the caller stops at
+  // t == rgs.
+  template <bool DEFER = false>
   __host__ __device__ __forceinline__ bool step(const uint32_t* __restrict__ tab,
                                                 const uint32_t* __restrict__ lds,
                                                 uint32_t levels, uint32_t budget, int pass,
-                                                M* slot, uint32_t& ms) {
+                                                M* slot, uint32_t& ms, M defer = 0) {
     ms = kInf;
     if (dead) return true;
     const M ALL = all_tools<N>();
@@ -358,7 +372,12 @@ struct Sim {
           const bool on_gpu = (gpum & bi) != 0;
           const uint32_t r = on_gpu ? umax32(g, c ? c + xw : 0u) : umax32(c, g ? g + xw : 0u);
           resolved |= bi;
-          if (!on_gpu) {
+          if (DEFER && ((defer >> i) & 1)) {
+            // prefix: modes of deferred tools are CPU, so the GPU ready time
+            // needs its own expression
+            rgs = umin32(rgs, umax32(g, c ? c + xw : 0u));
+            started |= bi;
+          } else if (!on_gpu) {
             const uint32_t f = r + rec[kToolCpu];
             T[i] = kTagCpu + f;
             started |= bi;
@@ -373,7 +392,7 @@ struct Sim {
         }
       }
     }
-    if (started == ALL) {
+    if (started == ALL && (!DEFER || rgs == kInf)) {
       ms = mk;
       return true;
     }
@@ -391,9 +410,59 @@ struct Sim {
     } else if (minq < kH) {
       next = umin32(next, minq);       // the next queued tool turns ready
     }
+    if (DEFER) next = umin32(next, rgs);
     if (next == kInf) return true;  // a queued tool can never fit: infeasible
     t = next;
     return false;
+  }
+
+  // After a DEFER prefix stopped at t == rgs, with the modes now set: give
+  // every deferred tool the prefix resolved the state the resolution step
+  // would have given it (its predecessors have all started, so their
+  // finishes are final).  Deferred tools still unresolved stay so, and the
+  // ordinary passes resolve them.
+  __host__ __device__ __forceinline__ void settle_deferred(const uint32_t* __restrict__ tab,
+                                                           M defer) {
+    const M gpum = gnm | gqm;
+    const Tab tp = fresh(tab);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if ((defer >> i) & 1) {
+        DEVMAP_KEEP_BRANCH();
+        const M bi = M(1) << i;
+        if (resolved & bi) {
+          const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
+          uint32_t g = 0, c = 0;
+#pragma unroll
+          for (int u = 0; u < i; ++u) {
+            if ((pm >> u) & 1) {
+              DEVMAP_KEEP_BRANCH();
+              const uint32_t f = T[u];
+              g = umax32(g, f < kH ? f : 0u);
+              c = umax32(c, f);
+            }
+          }
+          c = c >= kTagCpu ? c - kTagCpu : 0u;
+          const Tab rec = tp + (kHdrWords + kToolWords * i);
+          const uint32_t xw = rec[kToolXfer];
+          const bool on_gpu = (gpum & bi) != 0;
+          const uint32_t r = on_gpu ? umax32(g, c ? c + xw : 0u) : umax32(c, g ? g + xw : 0u);
+          if (!on_gpu) {
+            const uint32_t f = r + rec[kToolCpu];
+            T[i] = kTagCpu + f;
+            mk = umax32(mk, f);
+          } else {
+            started &= ~bi;
+            if (gnm & bi) {
+              T[i] = kTagNow + r;
+            } else {
+              T[i] = kTagQueue + r;
+              minq = umin32(minq, r);
+            }
+          }
+        }
+      }
+    }
   }
 };
 
@@ -950,23 +1019,53 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
 
   using S = typename std::conditional<SHARE, SimPS<N>, Sim<N>>::type;
   using SS = typename std::conditional<SHARE, SnapPS<N>, Snap<N>>::type;
-  constexpr int kPasses = SHARE ? 4 * N + 4 : 2 * N + 2;
-  // The prefix: inner tools on the CPU (their modes are never read before
-  // one of them is resolved).  pstar: the first pass that resolves one.
+  // (fixed at start: one pass more than a plain evaluation may take, the
+  // deferred tools' GPU ready time)
+  constexpr int kPasses = SHARE ? 4 * N + 4 : 2 * N + 4;
+  // Fixed at start, inner tools that are sinks with predecessors are
+  // deferred (Sim::step): the prefix runs on to their earliest GPU ready
+  // time.  The other inner tools ("early") stop it before the first pass
+  // that reads one of their modes, i.e. resolves one of them.
+  M defer = 0;
+  if constexpr (!SHARE) {
+    M has_succ = 0, has_pred = 0;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const M pm = load_mask<N>(tu, kHdrWords + kToolWords * i + kToolPredLo);
+      has_succ |= pm;
+      has_pred |= pm ? M(1) << i : M(0);
+    }
+    defer = inner & ~has_succ & has_pred;
+  }
+  const M early = inner & ~defer;
+  // The prefix: inner tools on the CPU (their modes are never read).
+  // pstar: the pass the inner combinations restart at.
   int pstar = -1;
   SS sm;
   {
     S sim;
     sim.init(tab, ogn, ogq);
     for (int pass = 0; pass < kPasses; ++pass) {
-      snap_save<N>(snap, sm, sim);
+      if (early) snap_save<N>(snap, sm, sim);
       uint32_t ms;
-      const bool fin = sim.step(tab, lds, levels, budget, pass, slot, ms);
-      if (first_read<N>(sim) & inner) {
-        pstar = pass;
+      bool fin;
+      if constexpr (SHARE) {
+        fin = sim.step(tab, lds, levels, budget, pass, slot, ms);
+      } else {
+        fin = sim.template step<true>(tab, lds, levels, budget, pass, slot, ms, defer);
+      }
+      if (first_read<N>(sim) & early) {
+        pstar = pass;  // restart this pass from the state saved before it
         break;
       }
       if (fin) break;  // out of memory or stuck before any inner tool: infeasible
+      if constexpr (!SHARE) {
+        if (sim.t >= sim.rgs) {  // the next pass is at a deferred tool's GPU ready time
+          snap_save<N>(snap, sm, sim);
+          pstar = pass + 1;
+          break;
+        }
+      }
     }
   }
   if (pstar < 0) return;  // every inner combination is infeasible
@@ -989,6 +1088,9 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
     sim.gnm = ogn | ign;
     sim.gqm = ogq | igq;
     sim.dead = ((sim.gnm | sim.gqm) & big) != 0;
+    if constexpr (!SHARE) {
+      if (defer) sim.settle_deferred(tab, defer);
+    }
     uint32_t ms = kInf;
     for (int pass = pstar; pass < kPasses; ++pass)
       if (sim.step(tab, lds, levels, budget, pass, slot, ms)) break;
