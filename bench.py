@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 65193600
-TRAFFIC_KERNEL_SHA256 = "41dffddf65446daff4aa8c5345455c8e5a89e1461bd2b8717be06e8489e5e3c7"
+TRAFFIC_BYTES = 74808066
+TRAFFIC_KERNEL_SHA256 = "48f7a3b69ae301d4ee1a339c1d682ed55e98f310259ba4cf755825258d27bd53"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 

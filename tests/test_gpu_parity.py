@@ -673,3 +673,44 @@ def test_shared_prefix_restarts_with_mixed_restart_passes(torch_cuda, O):
     P, Q = both(inst, O)
     say("shared-prefix plan, 3^16 tight")
     assert gpu_argmin(torch_cuda, P) == Q.argmin()
+
+
+def _deepest_two_kinds(inst):
+    """How the shared-prefix kernel treats the two inner tools of a full
+    search: "deferred" for a sink with predecessors, "early" otherwise."""
+    n = len(inst["tools"])
+    preds = [[] for _ in range(n)]
+    succ = [[] for _ in range(n)]
+    for u, v in inst["edges"]:
+        preds[v].append(u)
+        succ[u].append(v)
+    depth = [0] * n
+    for _ in range(n):
+        for u, v in inst["edges"]:
+            depth[v] = max(depth[v], depth[u] + 1)
+
+    def ancestors(v):
+        seen, todo = set(), list(preds[v])
+        while todo:
+            u = todo.pop()
+            if u not in seen:
+                seen.add(u)
+                todo += preds[u]
+        return len(seen)
+
+    late = sorted(range(n), key=lambda v: (-depth[v], -ancestors(v), v))[:2]
+    return ["deferred" if preds[v] and not succ[v] else "early" for v in late]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("shape,n,tight,seed", [
+    ("chain", 14, False, 8801), ("fanout", 14, True, 8802), ("random", 15, True, 8803),
+    ("random", 15, False, 8804), ("permuted", 15, True, 8805), ("permuted", 14, False, 8806)])
+def test_shared_prefix_deferred_inner_sinks(torch_cuda, O, shape, n, tight, seed):
+    """Full searches large enough for the shared-prefix plan, whose inner
+    tools are both deferred sinks, one deferred and one stopping the prefix
+    at its resolution (chains), or neither (fan-outs: sources)."""
+    inst = synth.random_instance(seed, n, shape, tight=tight)
+    P, Q = both(inst, O)
+    say(f"shared prefixes, {shape} {n} tight={tight}: inner tools {_deepest_two_kinds(inst)}")
+    assert gpu_argmin(torch_cuda, P) == Q.argmin()
