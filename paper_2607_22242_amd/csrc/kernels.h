@@ -791,6 +791,13 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
 template <int N>
 using IdxT = typename std::conditional<(N <= 20), uint32_t, uint64_t>::type;
 
+// Observer of every mapping a lane scores, called with (index, makespan or
+// kInf).  The kernels pass NoRecord, which compiles to nothing; a host-side
+// test harness records the makespans of a whole search.
+struct NoRecord {
+  __host__ __device__ __forceinline__ void operator()(uint64_t, uint32_t) const {}
+};
+
 // One lane's share of one work item: outer combination
 // outer_lo + item * kBlock + lane (the digits of enumeration positions J..N-1),
 // combined with every inner combination (positions 0..J-1) in range.  All
@@ -800,13 +807,13 @@ using IdxT = typename std::conditional<(N <= 20), uint32_t, uint64_t>::type;
 // index need not grow along the walk, so the running minimum compares
 // (makespan, index) in full.  Otherwise: index order, o * 3^J + i, clipped to
 // [lo, hi); indices grow, so a strict comparison keeps the lowest index.
-template <int N, bool FULL, bool SHARE>
+template <int N, bool FULL, bool SHARE, class Rec = NoRecord>
 __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
                                                      const uint32_t* __restrict__ tab,
                                                      const uint32_t* __restrict__ lds,
                                                      uint64_t item, uint32_t lane,
                                                      MaskT<N>* slot, uint32_t& best_ms,
-                                                     uint64_t& best_x) {
+                                                     uint64_t& best_x, Rec rec = Rec()) {
   using M = MaskT<N>;
   using I = IdxT<N>;
   const uint64_t rel = item * kBlock + lane;
@@ -847,6 +854,7 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
         ms = evaluate_sharing<N>(tab, lds, levels, budget, ogn | ign, ogq | igq, slot);
       else
         ms = evaluate<N>(tab, lds, levels, budget, ogn | ign, ogq | igq, slot);
+      rec(FULL ? uint64_t(xo + xi) : base + i, ms);
       if constexpr (FULL) {
         if (ms <= best_ms) {
           const I x = xo + xi;
@@ -993,13 +1001,14 @@ __host__ __device__ __forceinline__ MaskT<N> first_read(const SimPS<N>& sim) {
 // lane_search for a full range with shared prefixes (see above); the inner
 // positions 0..kSharedInner-1 hold the deepest tools.  SHARE: the
 // processor-sharing evaluator, whose saved state holds Y instead of T.
-template <int N, bool SHARE>
+template <int N, bool SHARE, class Rec = NoRecord>
 __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
                                                             const uint32_t* __restrict__ tab,
                                                             const uint32_t* __restrict__ lds,
                                                             uint64_t item, uint32_t lane,
                                                             MaskT<N>* slot, uint32_t* snap,
-                                                            uint32_t& best_ms, uint64_t& best_x) {
+                                                            uint32_t& best_ms, uint64_t& best_x,
+                                                            Rec rec = Rec()) {
   using M = MaskT<N>;
   using I = IdxT<N>;
   const uint64_t rel = item * kBlock + lane;
@@ -1094,6 +1103,7 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
     uint32_t ms = kInf;
     for (int pass = pstar; pass < kPasses; ++pass)
       if (sim.step(tab, lds, levels, budget, pass, slot, ms)) break;
+    rec(uint64_t(xo + xi), ms);
     if (ms <= best_ms) {
       const I x = xo + xi;
       if (ms < best_ms || x < bx) {
