@@ -903,7 +903,11 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // schedule of the other tools, and every event time, is the same for all
 // their modes: each lane runs that prefix once per outer combination, keeps
 // the state it had before the first pass that resolves an inner tool, and
-// restarts every inner combination from there.  The per-tool words go to LDS
+// restarts every inner combination from there.  With fixed-at-start
+// contention an inner tool that is a sink with predecessors (the deepest
+// tools are sinks) acts on no other tool before its GPU ready time, so it
+// does not stop the prefix when it is resolved: the prefix runs on to the
+// earliest such ready time (Sim::step<true>).  The per-tool words go to LDS
 // (one column per lane), the three masks to registers.  Tools up to
 // kPrefixMaxN.
 // Every tool's word is saved and restored, inner tools included (they are
