@@ -229,7 +229,8 @@ uint32_t table_levels(const sched_problem& p) {
 // each lane's schedule prefix once for all of their modes) and the next four
 // deepest on the lanes: the plain deepest-first order.
 bool prefix_plan(const sched_problem& p, uint64_t n_tables) {
-  if (p.n > kPrefixMaxN || p.enum_tools.size() < kSharedInner) return false;
+  if (p.n > (p.sharing ? kPrefixMaxNShare : kPrefixMaxN) || p.enum_tools.size() < kSharedInner)
+    return false;
   // enough lanes left to fill the GPU with kSharedInner inner digits
   const std::vector<int32_t>& v = p.late;
   uint64_t inner = 1;

@@ -26,7 +26,9 @@ constexpr int kMaxInnerDigits = 6;      // inner (wave-uniform) digits per lane
 #define DEVMAP_SHARED_INNER 2
 #endif
 constexpr uint32_t kSharedInner = DEVMAP_SHARED_INNER;  // inner digits of a shared-prefix search
-constexpr int kPrefixMaxN = 24;         // tool counts served by shared prefixes
+constexpr int kPrefixMaxN = 32;         // tool counts served by shared prefixes (fixed at start:
+                                        // N LDS words per lane)
+constexpr int kPrefixMaxNShare = 24;    // the same under processor sharing (2N words per lane)
 
 // Header words.
 enum : uint32_t {

@@ -909,7 +909,7 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // does not stop the prefix when it is resolved: the prefix runs on to the
 // earliest such ready time (Sim::step<true>).  The per-tool words go to LDS
 // (one column per lane), the three masks to registers.  Tools up to
-// kPrefixMaxN.
+// kPrefixMaxN (kPrefixMaxNShare under processor sharing).
 // Every tool's word is saved and restored, inner tools included (they are
 // 0): a branch per tool on the wave-uniform inner mask would be compiled as a
 // lane-mask test that the compiler computes inside the prefix loop and
@@ -917,7 +917,7 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 template <int N, bool SHARE>
 constexpr uint32_t snap_words() {
   // the per-tool words of the state (the masks and times stay in registers)
-  return N <= kPrefixMaxN ? (SHARE ? 2u : 1u) * uint32_t(N) : 1u;
+  return N <= (SHARE ? kPrefixMaxNShare : kPrefixMaxN) ? (SHARE ? 2u : 1u) * uint32_t(N) : 1u;
 }
 
 // A lane's saved schedule state: the per-tool words in its LDS column s, the
@@ -1147,15 +1147,17 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
 // block's minimum goes to partials[b].
 template <int N, bool FULL, bool SHARE>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
-    SHARE ? (FULL && N <= kPrefixMaxN ? (N <= 19 ? 4 : 3)  // LDS: 2N words per lane
+    SHARE ? (FULL && N <= kPrefixMaxNShare ? (N <= 19 ? 4 : 3)  // LDS: 2N words per lane
                                       : DEVMAP_SHARE_WAVES)
-          : (N <= 19 ? DEVMAP_SEARCH_WAVES_SMALL : DEVMAP_SEARCH_WAVES_LARGE)))) void
+          : (N <= 19 ? DEVMAP_SEARCH_WAVES_SMALL
+                     // from 27 tools the shared-prefix column leaves LDS for 4 blocks per CU
+                     : (FULL && N > 26 && N <= kPrefixMaxN ? 4 : DEVMAP_SEARCH_WAVES_LARGE))))) void
 search_kernel(SearchArgs a) {
   // the staged tables: lds_words_for(N, a.lds_levels) words, sized at launch
   extern __shared__ uint32_t s_lds[];
   __shared__ uint64_t s_wave_words[kBlock / 64];  // one 8-byte word per wave
   MaskT<N>* const slot = reinterpret_cast<MaskT<N>*>(&s_wave_words[threadIdx.x / 64]);
-  constexpr bool kPrefix = FULL && N <= kPrefixMaxN;
+  constexpr bool kPrefix = FULL && N <= (SHARE ? kPrefixMaxNShare : kPrefixMaxN);
   __shared__ uint32_t s_snap[kPrefix ? snap_words<N, SHARE>() * kBlock : 1];
   const uint32_t table = blockIdx.x / a.blocks_per_table;
   const uint32_t bb = blockIdx.x - table * a.blocks_per_table;

@@ -714,3 +714,20 @@ def test_shared_prefix_deferred_inner_sinks(torch_cuda, O, shape, n, tight, seed
     P, Q = both(inst, O)
     say(f"shared prefixes, {shape} {n} tight={tight}: inner tools {_deepest_two_kinds(inst)}")
     assert gpu_argmin(torch_cuda, P) == Q.argmin()
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("n,seed,tight", [(25, 8901, True), (28, 8902, False), (32, 8903, True)])
+def test_shared_prefix_wide_binary_spaces(torch_cuda, O, n, seed, tight):
+    """Full searches of 25- to 32-tool DAGs in GPU/CPU spaces of 2^22 mappings
+    (mixed with gpu_queue-only and CPU-only tools), large enough for the
+    shared-prefix plan with 64-bit indices, against the oracle."""
+    inst = synth.random_instance(seed, n, "permuted", tight=tight)
+    allowed = ([3] * 22 + [1] * (n - 22 - 1) + [4])  # gpu_now|cpu; cpu only; gpu_queue only
+    P = S.Problem.from_instance(inst, allowed)
+    Q = O.Problem.from_instance(inst)
+    sp = O.Space(allowed)
+    assert P.n_mappings == sp.size() == 1 << 22
+    say(f"shared prefixes, binary space, {n} tools tight={tight}")
+    bi, bm = gpu_argmin(torch_cuda, P)
+    assert (bi, bm) == O.masked_argmin(Q, sp)
