@@ -78,14 +78,19 @@ def test_shared_prefix_plan_matches_oracle(host_search, oracle_mod, shape, n, ti
     assert got == oracle_mod.Problem.from_instance(inst).argmin()
 
 
-@pytest.mark.parametrize("shape,tight,seed", [
-    ("chain", True, 8811), ("random", True, 8812), ("permuted", False, 8813),
-    ("fanout", False, 8814)])
+@pytest.mark.parametrize("shape,tight,seed,fits", [
+    ("chain", True, 8811, False), ("random", True, 8812, False),
+    ("permuted", False, 8813, False), ("fanout", False, 8814, False),
+    ("fanout", False, 8815, True), ("random", False, 8816, True)])
 def test_shared_prefix_every_mapping_matches_oracle(host_search, oracle_mod, tmp_path,
-                                                   shape, tight, seed):
+                                                   shape, tight, seed, fits):
     """Every one of the 3^14 makespans a shared-prefix search scores, not only
-    the winner, against the oracle's (infeasible: 0xFFFFFFFF)."""
+    the winner, against the oracle's (infeasible: 0xFFFFFFFF).  fits: the
+    budget is the summed footprint, so VRAM never binds (the kernels then
+    skip the VRAM sums)."""
     inst = synth.random_instance(seed, 14, shape, tight=tight)
+    if fits:
+        inst["vram_budget_mib"] = sum(t[4] for t in inst["tools"])
     path = str(tmp_path / "ms.bin")
     _, prefix = host_search(inst, path)
     assert prefix == 1
