@@ -702,7 +702,6 @@ def _deepest_two_kinds(inst):
     return ["deferred" if preds[v] and not succ[v] else "early" for v in late]
 
 
-@pytest.mark.gpu
 @pytest.mark.parametrize("shape,n,tight,seed", [
     ("chain", 14, False, 8801), ("fanout", 14, True, 8802), ("random", 15, True, 8803),
     ("random", 15, False, 8804), ("permuted", 15, True, 8805), ("permuted", 14, False, 8806)])
@@ -716,7 +715,6 @@ def test_shared_prefix_deferred_inner_sinks(torch_cuda, O, shape, n, tight, seed
     assert gpu_argmin(torch_cuda, P) == Q.argmin()
 
 
-@pytest.mark.gpu
 @pytest.mark.parametrize("n,seed,tight", [(25, 8901, True), (28, 8902, False), (32, 8903, True)])
 def test_shared_prefix_wide_binary_spaces(torch_cuda, O, n, seed, tight):
     """Full searches of 25- to 32-tool DAGs in GPU/CPU spaces of 2^22 mappings
@@ -731,3 +729,20 @@ def test_shared_prefix_wide_binary_spaces(torch_cuda, O, n, seed, tight):
     say(f"shared prefixes, binary space, {n} tools tight={tight}")
     bi, bm = gpu_argmin(torch_cuda, P)
     assert (bi, bm) == O.masked_argmin(Q, sp)
+
+
+@pytest.mark.parametrize("n,seed", [(27, 9960), (31, 9961)])
+def test_pruned_search_wide_masked(torch_cuda, O, n, seed):
+    """The pruned search on 27- and 31-tool DAGs in 2^21-mapping spaces (its
+    subspace launches take the shared-prefix kernel beyond 24 tools), against
+    the oracle's masked search."""
+    inst = synth.random_instance(seed, n, "permuted", tight=True)
+    allowed = [3] * 21 + [1] * (n - 21)
+    P = S.Problem.from_instance(inst, allowed)
+    Q = O.Problem.from_instance(inst)
+    sp = O.Space(allowed)
+    assert P.n_mappings == sp.size() == 1 << 21
+    bi, bm, st = pruned(P)
+    say(f"pruned wide masked n={n}: {st}")
+    assert (bi, bm) == O.masked_argmin(Q, sp)
+    assert gpu_argmin(torch_cuda, P) == (bi, bm)
