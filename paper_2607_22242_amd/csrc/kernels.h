@@ -1002,9 +1002,116 @@ __host__ __device__ __forceinline__ MaskT<N> first_read(const SimPS<N>& sim) {
   return sim.readym;
 }
 
-// lane_search for a full range with shared prefixes (see above); the inner
-// positions 0..kSharedInner-1 hold the deepest tools.  SHARE: the
-// processor-sharing evaluator, whose saved state holds Y instead of T.
+// Cross-lane helpers of the shared-prefix search.  A host build has one lane
+// per "wave": the ballot is the lane's own flag, its rank 0, and a pull from
+// lane 0 returns the lane's own value.
+__host__ __device__ __forceinline__ uint32_t lane_in_wave(uint32_t lane) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return lane & 63u;
+#else
+  (void)lane;
+  return 0u;
+#endif
+}
+
+// Lanes of a wave (one in a host build).
+__host__ __device__ constexpr uint32_t wave_lanes() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return 64u;
+#else
+  return 1u;
+#endif
+}
+
+__host__ __device__ __forceinline__ uint64_t wave_ballot(bool p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __ballot(p);
+#else
+  return p ? 1u : 0u;
+#endif
+}
+
+// Number of lanes below the calling one whose bit is set in v.
+__host__ __device__ __forceinline__ uint32_t lanes_below(uint64_t v) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_amdgcn_mbcnt_hi(uint32_t(v >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(v), 0u));
+#else
+  (void)v;
+  return 0u;
+#endif
+}
+
+// x of lane src (every lane of the wave must be active).
+__host__ __device__ __forceinline__ uint32_t pull(uint32_t x, uint32_t src) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return uint32_t(__builtin_amdgcn_ds_bpermute(int(src << 2), int(x)));
+#else
+  (void)src;
+  return x;
+#endif
+}
+
+// x of this lane delivered to lane dst; dst must be a permutation of the
+// wave's lanes (every lane active).
+__host__ __device__ __forceinline__ uint32_t push(uint32_t x, uint32_t dst) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return uint32_t(__builtin_amdgcn_ds_permute(int(dst << 2), int(x)));
+#else
+  (void)dst;
+  return x;
+#endif
+}
+
+__host__ __device__ __forceinline__ uint64_t pull64(uint64_t x, uint32_t src) {
+  return uint64_t(pull(uint32_t(x), src)) | (uint64_t(pull(uint32_t(x >> 32), src)) << 32);
+}
+
+template <class M>
+__host__ __device__ __forceinline__ M pull_mask(M x, uint32_t src) {
+  if constexpr (sizeof(M) == 4) return pull(x, src);
+  else return pull64(x, src);
+}
+
+// The register part of lane src's saved state.
+template <int N>
+__host__ __device__ __forceinline__ Snap<N> pull_snap(const Snap<N>& m, uint32_t src) {
+  Snap<N> r;
+  r.started = pull_mask(m.started, src);
+  r.resolved = pull_mask(m.resolved, src);
+  r.run = pull_mask(m.run, src);
+  r.t = pull(m.t, src);
+  r.qfin = pull(m.qfin, src);
+  r.minq = pull(m.minq, src);
+  r.mk = pull(m.mk, src);
+  return r;
+}
+
+template <int N>
+__host__ __device__ __forceinline__ SnapPS<N> pull_snap(const SnapPS<N>& m, uint32_t src) {
+  SnapPS<N> r;
+  r.running = pull_mask(m.running, src);
+  r.done = pull_mask(m.done, src);
+  r.V = pull64(m.V, src);
+  r.t = pull(m.t, src);
+  return r;
+}
+
+// Full-range search with shared schedule prefixes (see above), one work item
+// of a wave: the inner positions 0..kSharedInner-1 hold the deepest tools.
+// SHARE: the processor-sharing evaluator, whose saved state holds Y instead
+// of T.
+//
+// Phase 1: every lane runs the prefix of its outer combination and saves its
+// state (the per-tool words in its LDS column, the rest in registers).
+// Phase 2: the (prefix, inner combination) pairs of the wave's feasible
+// prefixes are dealt to the lanes in rounds of 64, the inner combinations of
+// one prefix in consecutive lanes: lane l of round r takes pair 64r + l, i.e.
+// prefix (64r + l) / C (C inner combinations) and combination (64r + l) % C,
+// restores that prefix's state from its owner (LDS column and register
+// pulls) and runs the rest of the schedule.  Lanes of a round thus share few
+// prefixes, so the wave-wide masks of a pass stay narrow, and lanes whose
+// prefix is infeasible take no round.  Every lane of the wave must call this
+// function for the same item (lanes beyond the range take part in the pulls).
 template <int N, bool SHARE, class Rec = NoRecord>
 __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
                                                             const uint32_t* __restrict__ tab,
@@ -1016,13 +1123,12 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
   using M = MaskT<N>;
   using I = IdxT<N>;
   const uint64_t rel = item * kBlock + lane;
-  if (rel >= a.n_outer) return;
+  const uint32_t wl = lane_in_wave(lane);
+  uint32_t* const snap0 = snap - wl;  // LDS column of the wave's lane 0
   const uint32_t levels = tab[kHdrLevels];
   const uint32_t budget = tab[kHdrBudget];
   constexpr uint32_t J = kSharedInner;
-  M ogn, ogq;
-  uint64_t xo64;
-  decode_positions<N>(tab, a.outer_lo + rel, J, tab[kHdrPositions], ogn, ogq, xo64);
+  static_assert(J >= 1 && J <= 2, "the pairs are dealt for one or two inner digits");
   // The inner tools (a wave-uniform mask, read through scalar loads).
   const Tab tu{tab};
   M inner = 0;
@@ -1051,11 +1157,16 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
     defer = inner & ~has_succ & has_pred;
   }
   const M early = inner & ~defer;
-  // The prefix: inner tools on the CPU (their modes are never read).
-  // pstar: the pass the inner combinations restart at.
+
+  // Phase 1.  pstar: the pass the inner combinations restart at (-1: none,
+  // the prefix is infeasible or the lane is beyond the range).
+  M ogn = 0, ogq = 0;
+  uint64_t xo64 = 0;
   int pstar = -1;
-  SS sm;
-  {
+  SS sm{};
+  if (rel < a.n_outer) {
+    decode_positions<N>(tab, a.outer_lo + rel, J, tab[kHdrPositions], ogn, ogq, xo64);
+    // The prefix: inner tools on the CPU (their modes are never read).
     S sim;
     sim.init(tab, ogn, ogq);
     for (int pass = 0; pass < kPasses; ++pass) {
@@ -1081,61 +1192,66 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
       }
     }
   }
-  if (pstar < 0) return;  // every inner combination is infeasible
 
+  // Phase 2: deal the (prefix, inner combination) pairs.  own: lane of the
+  // rank-th feasible prefix, delivered to lane `rank` by one permutation
+  // (infeasible lanes fill the lanes from nv on).
+  const uint64_t feas = wave_ballot(pstar >= 0);
+  const uint32_t nv = uint32_t(__builtin_popcountll(feas));
+  const uint32_t rk = lanes_below(feas);
+  const uint32_t owner_of_rank = push(wl, pstar >= 0 ? rk : nv + wl - rk);
+  // Inner combinations: C of them, positions 0 and 1 of radices r0, r1.
+  const uint32_t C = a.inner_count;
+  const uint32_t o0 = tab[kEnumOptBase + 0], o1 = J > 1 ? tab[kEnumOptBase + 1] : 0u;
+  const uint32_t r0 = opt_radix(o0);
+  const M b0 = M(1) << tab[kEnumLabBase + 0];
+  const M b1 = J > 1 ? M(1) << tab[kEnumLabBase + 1] : M(0);
+  const I w0 = I(uint64_t(tab[kEnumWeightBase + 0]) | (uint64_t(tab[kEnumWeightBase + 1]) << 32));
+  const I w1 = J > 1 ? I(uint64_t(tab[kEnumWeightBase + 2]) | (uint64_t(tab[kEnumWeightBase + 3]) << 32))
+                     : I(0);
+  const uint32_t pairs = nv * C;
+  constexpr uint32_t W = wave_lanes();
+  // pair index of this lane in the first round, as (prefix rank, combination)
+  uint32_t q = wl / C, c = wl - (wl / C) * C;
+  const uint32_t qW = W / C, cW = W - qW * C;
   I bx = I(best_x);
-  const I xo = I(xo64);
-  M ign = 0, igq = 0;
-  uint32_t idig = 0;
-  I xi = 0;
-#pragma unroll
-  for (uint32_t j = 0; j < J; ++j) {
-    const uint32_t m = opt_mode(tab[kEnumOptBase + j], 0u);
-    const M b = M(1) << tab[kEnumLabBase + j];
-    if (m == 1u) ign |= b;
-    if (m == 2u) igq |= b;
-  }
-  for (uint32_t i = 0; i < a.inner_count; ++i) {
-    S sim;
-    snap_load<N>(snap, sm, sim);
-    sim.gnm = ogn | ign;
-    sim.gqm = ogq | igq;
-    sim.dead = ((sim.gnm | sim.gqm) & big) != 0;
-    if constexpr (!SHARE) {
-      if (defer) sim.settle_deferred(tab, defer);
-    }
-    uint32_t ms = kInf;
-    for (int pass = pstar; pass < kPasses; ++pass)
-      if (sim.step(tab, lds, levels, budget, pass, slot, ms)) break;
-    rec(uint64_t(xo + xi), ms);
-    if (ms <= best_ms) {
-      const I x = xo + xi;
-      if (ms < best_ms || x < bx) {
-        best_ms = ms;
-        bx = x;
+  for (uint32_t r0i = 0; r0i < pairs; r0i += W) {
+    const uint32_t src = pull(owner_of_rank, q < W ? q : 0u);
+    const SS ss = pull_snap<N>(sm, src);
+    const M sgn = pull_mask(ogn, src), sgq = pull_mask(ogq, src);
+    const I sxo = I(pull(uint32_t(xo64), src)) |
+                  I(sizeof(I) > 4 ? (uint64_t(pull(uint32_t(xo64 >> 32), src)) << 32) : 0u);
+    const int sps = int(pull(uint32_t(pstar), src));
+    if (r0i + wl < pairs) {
+      // digits of combination c: d0 = c mod r0, d1 = c div r0
+      const uint32_t d1 = c >= r0 ? (c >= 2u * r0 ? 2u : 1u) : 0u;
+      const uint32_t d0 = c - d1 * r0;
+      const uint32_t m0 = opt_mode(o0, d0), m1 = J > 1 ? opt_mode(o1, d1) : 0u;
+      S sim;
+      snap_load<N>(snap0 + src, ss, sim);
+      sim.gnm = sgn | (m0 == 1u ? b0 : M(0)) | (m1 == 1u ? b1 : M(0));
+      sim.gqm = sgq | (m0 == 2u ? b0 : M(0)) | (m1 == 2u ? b1 : M(0));
+      sim.dead = ((sim.gnm | sim.gqm) & big) != 0;
+      if constexpr (!SHARE) {
+        if (defer) sim.settle_deferred(tab, defer);
+      }
+      const I x = sxo + I(d0) * w0 + I(d1) * w1;
+      uint32_t ms = kInf;
+      for (int pass = sps; pass < kPasses; ++pass)
+        if (sim.step(tab, lds, levels, budget, pass, slot, ms)) break;
+      rec(uint64_t(x), ms);
+      if (ms <= best_ms) {
+        if (ms < best_ms || x < bx) {
+          best_ms = ms;
+          bx = x;
+        }
       }
     }
-    // odometer step on the inner digits
-#pragma unroll
-    for (uint32_t j = 0; j < J; ++j) {
-      const uint32_t o = tab[kEnumOptBase + j];
-      const uint32_t d = (idig >> (2u * j)) & 3u;
-      const M b = M(1) << tab[kEnumLabBase + j];
-      const I w = I(uint64_t(tab[kEnumWeightBase + 2 * j]) |
-                    (uint64_t(tab[kEnumWeightBase + 2 * j + 1]) << 32));
-      ign &= ~b;
-      igq &= ~b;
-      const bool carry = d + 1u == opt_radix(o);
-      const uint32_t m = opt_mode(o, carry ? 0u : d + 1u);
-      if (m == 1u) ign |= b;
-      if (m == 2u) igq |= b;
-      if (!carry) {
-        idig += 1u << (2u * j);
-        xi += w;
-        break;
-      }
-      idig &= ~(3u << (2u * j));
-      xi -= I(d) * w;
+    q += qW;
+    c += cW;
+    if (c >= C) {
+      c -= C;
+      q += 1u;
     }
   }
   if (best_ms != kInf) best_x = bx;
