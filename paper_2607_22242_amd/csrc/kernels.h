@@ -91,7 +91,9 @@ __host__ __device__ __forceinline__ bool bit(MaskT<N> m, int v) {
 
 // LDS image staged by every block: footprints by internal label, then the
 // internal label of every original tool, then the duration table (its
-// length follows the problem's contention levels).
+// length follows the problem's contention levels), level-major:
+// dur[(level - 1) * 2N + 2 * label + q] (q = 0 gpu_now, 1 gpu_queue), so a
+// pass finds its row once and each start reads one word at a fixed offset.
 template <int N>
 constexpr uint32_t lds_levels() { return N < kMaxLevels ? N : kMaxLevels; }
 template <int N>
@@ -329,6 +331,7 @@ struct Sim {
       }
     }
     const uint32_t lev = umin32(umax32(k, 1u), levels) - 1u;
+    const uint32_t* const s_row = s_dur + lev * (2u * uint32_t(N));  // durations at level lev + 1
 
     // B. starts, resolution, next event
     uint32_t tn = kInf;
@@ -340,7 +343,7 @@ struct Sim {
       if ((ww_b >> i) & 1) {
         const bool adm = (hsel == uint32_t(i));
         if (T[i] == now_t || adm) {
-          const uint32_t d = s_dur[(uint32_t(i) * 2u + (adm ? 1u : 0u)) * levels + lev];
+          const uint32_t d = s_row[2u * uint32_t(i) + (adm ? 1u : 0u)];
           T[i] = t + d;
           started |= bi;
           run |= bi;
@@ -726,16 +729,27 @@ __device__ __forceinline__ void block_min(uint32_t& ms, uint64_t& x) {
   }
 }
 
+// Words [first, first + stride, ...) of the LDS image of table tab.  The
+// table's duration table is label-major, dur[(2 * label + q) * levels +
+// level - 1]; the image is level-major (see lds_dur_off).
 template <int N>
-__device__ __forceinline__ void stage_tables(const uint32_t* tab, uint32_t* lds) {
+__host__ __device__ __forceinline__ void stage_image(const uint32_t* tab, uint32_t* lds,
+                                                     uint32_t first, uint32_t stride) {
   const uint32_t levels = tab[kHdrLevels];
   const uint32_t* dur = tab + tab[kHdrDurOff];
-  for (uint32_t i = threadIdx.x; i < uint32_t(N) * 2u * levels; i += blockDim.x)
-    lds[lds_dur_off<N>() + i] = dur[i];
-  for (uint32_t i = threadIdx.x; i < uint32_t(N); i += blockDim.x) {
+  for (uint32_t w = first; w < uint32_t(N) * 2u * levels; w += stride) {
+    const uint32_t lev = w / (2u * uint32_t(N)), iq = w - lev * (2u * uint32_t(N));
+    lds[lds_dur_off<N>() + w] = dur[iq * levels + lev];
+  }
+  for (uint32_t i = first; i < uint32_t(N); i += stride) {
     lds[lds_mem_off<N>() + i] = tab[kHdrWords + kToolWords * i + kToolMem];
     lds[lds_pos_off<N>() + i] = tab[kPosBase + i];
   }
+}
+
+template <int N>
+__device__ __forceinline__ void stage_tables(const uint32_t* tab, uint32_t* lds) {
+  stage_image<N>(tab, lds, threadIdx.x, blockDim.x);
   __syncthreads();
 }
 

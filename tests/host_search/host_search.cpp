@@ -53,14 +53,8 @@ static void run(const sched_problem* p, const char* table_path) {
   set_enumeration(*p, enumeration(*p, true, int(a.inner_digits), a.prefix != 0), table.data());
   const uint32_t* tab = table.data();
   // the block's LDS image (stage_tables)
-  const uint32_t levels = tab[kHdrLevels];
-  std::vector<uint32_t> lds(lds_words_for(N, levels));
-  const uint32_t* dur = tab + tab[kHdrDurOff];
-  for (uint32_t i = 0; i < uint32_t(N) * 2u * levels; ++i) lds[lds_dur_off<N>() + i] = dur[i];
-  for (uint32_t i = 0; i < uint32_t(N); ++i) {
-    lds[lds_mem_off<N>() + i] = tab[kHdrWords + kToolWords * i + kToolMem];
-    lds[lds_pos_off<N>() + i] = tab[kPosBase + i];
-  }
+  std::vector<uint32_t> lds(lds_words_for(N, tab[kHdrLevels]));
+  stage_image<N>(tab, lds.data(), 0, 1);
   uint32_t gms = kInf;
   uint64_t gx = ~0ull;
 #pragma omp parallel
