@@ -164,6 +164,18 @@ int sched_bruteforce_argmin(const sched_problem *p, uint64_t lo, uint64_t hi,
                             void *d_workspace, size_t ws_bytes, void *hip_stream,
                             sched_result *h_out);
 
+/* Diagnostic for parity tests, not part of the method: the full-range search
+ * of sched_bruteforce_argmin over [0, number of mappings), with the same plan
+ * and kernels (shared schedule prefixes included), that also writes the
+ * makespan of every mapping it scores to d_makespan[index] (device, uint32,
+ * 0xFFFFFFFF when infeasible).  Every mapping is scored exactly once, so each
+ * entry is written once.  capacity: entries of d_makespan, at least the
+ * number of mappings (else SCHED_E_WORKSPACE); d_workspace as for
+ * sched_bruteforce_argmin.  *h_out receives the search result. */
+int sched_bruteforce_record(const sched_problem *p, void *d_workspace, size_t ws_bytes,
+                            void *hip_stream, uint32_t *d_makespan, uint64_t capacity,
+                            sched_result *h_out);
+
 /* Batched re-scoring of perturbed profiles (the running-average feedback of
  * Section 3.2): replica r is problem replica_problem[r] with the latencies
  * replica_lat[off_r .. off_r + N_r), where off_r is the sum of N over the

@@ -27,6 +27,7 @@ EXPORTED = ["sched_problem_create", "sched_problem_create_masked", "sched_proble
             "sched_problem_destroy",
             "sched_mapping_modes", "sched_mapping_index", "sched_num_tools",
             "sched_num_mappings", "sched_workspace_bytes", "sched_bruteforce_argmin",
+            "sched_bruteforce_record",
             "sched_eval_batch", "sched_eval_mappings", "sched_eval_reprobes",
             "sched_pruned_workspace_bytes", "sched_pruned_argmin",
             "sched_monitor_create", "sched_monitor_destroy", "sched_monitor_observe",
@@ -119,6 +120,9 @@ def lib():
         L.sched_bruteforce_argmin.restype = ctypes.c_int
         L.sched_bruteforce_argmin.argtypes = [P, ctypes.c_uint64, ctypes.c_uint64, P,
                                               ctypes.c_size_t, P, ctypes.POINTER(sched_result)]
+        L.sched_bruteforce_record.restype = ctypes.c_int
+        L.sched_bruteforce_record.argtypes = [P, P, ctypes.c_size_t, P, P, ctypes.c_uint64,
+                                              ctypes.POINTER(sched_result)]
         L.sched_eval_batch.restype = ctypes.c_int
         L.sched_eval_batch.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32, P,
                                        ctypes.c_size_t, P, P]
@@ -269,6 +273,19 @@ def sched_bruteforce_argmin(handle, lo: int, hi: int, workspace, stream=None) ->
     wp, wb = _ws(workspace)
     _check(lib().sched_bruteforce_argmin(handle, lo, hi, wp, wb, _stream_ptr(stream),
                                          ctypes.byref(out)), "sched_bruteforce_argmin")
+    return out.best_index, out.makespan_us
+
+
+def sched_bruteforce_record(handle, workspace, d_makespan, stream=None) -> Tuple[int, int]:
+    """Full-range search that also writes every mapping's makespan into the
+    uint32/int32 device tensor d_makespan (index order, 0xFFFFFFFF
+    infeasible); returns (best_index, makespan_us)."""
+    assert d_makespan.element_size() == 4 and d_makespan.is_contiguous()
+    out = sched_result()
+    wp, wb = _ws(workspace)
+    _check(lib().sched_bruteforce_record(handle, wp, wb, _stream_ptr(stream),
+                                         d_makespan.data_ptr(), d_makespan.numel(),
+                                         ctypes.byref(out)), "sched_bruteforce_record")
     return out.best_index, out.makespan_us
 
 

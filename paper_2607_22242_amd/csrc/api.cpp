@@ -691,6 +691,44 @@ int sched_bruteforce_argmin(const sched_problem* p, uint64_t lo, uint64_t hi, vo
   return SCHED_OK;
 }
 
+int sched_bruteforce_record(const sched_problem* p, void* d_workspace, size_t ws_bytes,
+                            void* hip_stream, uint32_t* d_makespan, uint64_t capacity,
+                            sched_result* h_out) {
+  if (p == nullptr || h_out == nullptr || d_makespan == nullptr) return SCHED_E_NULL;
+  if (capacity < p->n_mappings) return SCHED_E_WORKSPACE;
+  const Layout L = layout_for(size_t(p->table_words) * 4, partial_capacity(1), 1);
+  int rc = check_workspace(d_workspace, ws_bytes, L.total);
+  if (rc != SCHED_OK) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  char* ws = static_cast<char*>(d_workspace);
+
+  SearchArgs a{};
+  plan_search(*p, 0, p->n_mappings, 1, a);
+  a.tables = reinterpret_cast<const uint32_t*>(ws + L.tables);
+  a.table_stride = p->table_words;
+  a.partials = reinterpret_cast<Partial*>(ws + L.partials);
+  a.record = d_makespan;
+  DevResult* d_res = reinterpret_cast<DevResult*>(ws + L.results);
+
+  std::vector<uint32_t> table;
+  try {
+    table = p->table;
+  } catch (const std::bad_alloc&) {
+    return SCHED_E_NOMEM;
+  }
+  set_enumeration(*p, enumeration(*p, true, int(a.inner_digits), a.prefix != 0), table.data());
+  HIP_TRY(hipMemcpyAsync(ws + L.tables, table.data(), size_t(p->table_words) * 4,
+                         hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_search(p->n, a, s));
+  HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, 1, d_res, s));
+  DevResult r;
+  HIP_TRY(hipMemcpyAsync(&r, d_res, sizeof(r), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  h_out->best_index = r.index;
+  h_out->makespan_us = r.makespan;
+  return SCHED_OK;
+}
+
 int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
                      const int32_t* replica_problem, const sched_lat* replica_lat,
                      int32_t n_replicas, void* d_workspace, size_t ws_bytes, void* hip_stream,

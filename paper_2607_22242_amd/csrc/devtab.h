@@ -124,6 +124,8 @@ struct SearchArgs {
   uint32_t prefix;            // 1: shared prefixes (kSharedInner inner digits on the
                               //    deepest tools, full range, fixed at start)
   uint32_t lds_levels;        // the most contention levels any of the tables stores
+  uint32_t* record;           // full range, one table: every scored mapping's makespan
+                              // (kInf if infeasible) goes to record[index]; null: none
 };
 
 struct DevResult {

@@ -806,10 +806,23 @@ template <int N>
 using IdxT = typename std::conditional<(N <= 20), uint32_t, uint64_t>::type;
 
 // Observer of every mapping a lane scores, called with (index, makespan or
-// kInf).  The kernels pass NoRecord, which compiles to nothing; a host-side
-// test harness records the makespans of a whole search.
+// kInf).  Partial-range searches pass NoRecord, which compiles to nothing;
+// full-range searches pass RecordTo, which writes only in a diagnostic run
+// (sched_bruteforce_record); a host-side test harness records the makespans
+// of a whole search through the same hook.
 struct NoRecord {
+  __host__ __device__ __forceinline__ bool on() const { return false; }
   __host__ __device__ __forceinline__ void operator()(uint64_t, uint32_t) const {}
+};
+
+// The search kernels' observer: writes (index, makespan) to out[index] when
+// out is set (a diagnostic run), else nothing (one wave-uniform test).
+struct RecordTo {
+  uint32_t* out;
+  __host__ __device__ __forceinline__ bool on() const { return out != nullptr; }
+  __host__ __device__ __forceinline__ void operator()(uint64_t x, uint32_t ms) const {
+    if (out != nullptr) out[x] = ms;
+  }
 };
 
 // One lane's share of one work item: outer combination
@@ -1229,6 +1242,14 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
   uint32_t q = wl / C, c = wl - (wl / C) * C;
   const uint32_t qW = W / C, cW = W - qW * C;
   I bx = I(best_x);
+  if (rec.on() && pstar < 0 && rel < a.n_outer) {
+    // an infeasible prefix: every inner combination is infeasible
+    for (uint32_t cc = 0; cc < C; ++cc) {
+      const uint32_t d1 = cc >= r0 ? (cc >= 2u * r0 ? 2u : 1u) : 0u;
+      const uint32_t d0 = cc - d1 * r0;
+      rec(uint64_t(I(xo64) + I(d0) * w0 + I(d1) * w1), kInf);
+    }
+  }
   for (uint32_t r0i = 0; r0i < pairs; r0i += W) {
     const uint32_t src = pull(owner_of_rank, q < W ? q : 0u);
     const SS ss = pull_snap<N>(sm, src);
@@ -1296,20 +1317,23 @@ search_kernel(SearchArgs a) {
 
   uint32_t best_ms = kInf;
   uint64_t best_x = ~0ull;
+  using Rec = typename std::conditional<FULL, RecordTo, NoRecord>::type;
+  Rec rec{};
+  if constexpr (FULL) rec.out = a.record;
   if constexpr (kPrefix) {
     if (a.prefix) {
       for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-        lane_search_prefix<N, SHARE>(a, tab, s_lds, item, threadIdx.x, slot,
-                                     s_snap + threadIdx.x, best_ms, best_x);
+        lane_search_prefix<N, SHARE, Rec>(a, tab, s_lds, item, threadIdx.x, slot,
+                                          s_snap + threadIdx.x, best_ms, best_x, rec);
     } else {
       for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-        lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x,
-                                    slot, best_ms, best_x);
+        lane_search<N, FULL, SHARE, Rec>(a, tab, s_lds, item, threadIdx.x,
+                                         slot, best_ms, best_x, rec);
     }
   } else {
     for (uint64_t item = bb; item < a.items_per_table; item += a.blocks_per_table)
-      lane_search<N, FULL, SHARE>(a, tab, s_lds, item, threadIdx.x, slot,
-                                  best_ms, best_x);
+      lane_search<N, FULL, SHARE, Rec>(a, tab, s_lds, item, threadIdx.x, slot,
+                                       best_ms, best_x, rec);
   }
 
   block_min(best_ms, best_x);

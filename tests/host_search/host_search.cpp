@@ -40,12 +40,14 @@ using namespace devmap;
 // Stores each scored mapping's makespan at its index.
 struct Table {
   uint32_t* ms;
+  bool on() const { return true; }
   void operator()(uint64_t x, uint32_t m) const { ms[x] = m; }
 };
 
 template <int N>
 static void run(const sched_problem* p, const char* table_path) {
-  std::vector<uint32_t> all(table_path ? p->n_mappings : 0, kInf);
+  // unwritten entries keep a value no makespan or infeasible mark takes
+  std::vector<uint32_t> all(table_path ? p->n_mappings : 0, 0xFFFFFFFEu);
   const Table rec{all.data()};
   SearchArgs a{};
   plan_search(*p, 0, p->n_mappings, 1, a);

@@ -92,6 +92,18 @@ def test_workspace_and_range_validation_before_any_device_work():
     assert err(r, 0, 3 ** 8, FakeWs(0, nbytes)) == "SCHED_E_WORKSPACE"
     assert err(r, 0, 3 ** 8, FakeWs(128, nbytes)) == "SCHED_E_WORKSPACE"
     assert err(r, 0, 3 ** 8, FakeWs(256, nbytes - 256)) == "SCHED_E_WORKSPACE"
+    rec = lambda ws, out: S.sched_bruteforce_record(P.handle, ws, out, fs)  # noqa: E731
+
+    class FakeOut(FakeWs):
+        def element_size(self):
+            return 4
+
+        def is_contiguous(self):
+            return True
+
+    assert err(rec, FakeWs(256, nbytes), FakeOut(256, 3 ** 8 - 1)) == "SCHED_E_WORKSPACE"
+    assert err(rec, FakeWs(128, nbytes), FakeOut(256, 3 ** 8)) == "SCHED_E_WORKSPACE"
+    assert err(rec, FakeWs(256, nbytes), FakeOut(0, 3 ** 8)) == "SCHED_E_NULL"
     b = lambda rp, ws: S.sched_eval_batch([P.handle], rp, [synth.load(0)["tools"]], ws, fs)  # noqa
     assert err(b, [1], FakeWs(256, 1 << 30)) == "SCHED_E_RANGE"
     assert err(b, [0], FakeWs(256, 64)) == "SCHED_E_WORKSPACE"
