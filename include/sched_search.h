@@ -164,6 +164,21 @@ int sched_bruteforce_argmin(const sched_problem *p, uint64_t lo, uint64_t hi,
                             void *d_workspace, size_t ws_bytes, void *hip_stream,
                             sched_result *h_out);
 
+/* For callers that cannot allocate device memory or pass a workspace (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): sched_bruteforce_argmin without a workspace argument.  The
+ * table, block partials and result live in a fixed per-GPU array of the
+ * library (2 MiB, held by each GPU the library runs on until the process
+ * ends); the call allocates nothing (no hipMalloc, hipFree or heap memory).
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (several host threads or streams at once) race and must be serialized by
+ * the caller.  Nothing in the array needs to start at zero: each call writes
+ * what it reads.  Errors as for sched_bruteforce_argmin; SCHED_E_WORKSPACE if
+ * the problem's table and partials do not fit the array (never for problems
+ * sched_problem_create accepts). */
+int sched_bruteforce_argmin_noalloc(const sched_problem *p, uint64_t lo, uint64_t hi,
+                                    void *hip_stream, sched_result *h_out);
+
 /* Diagnostic for parity tests, not part of the method: the full-range search
  * of sched_bruteforce_argmin over [0, number of mappings), with the same plan
  * and kernels (shared schedule prefixes included), that also writes the

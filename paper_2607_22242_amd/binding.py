@@ -27,7 +27,7 @@ EXPORTED = ["sched_problem_create", "sched_problem_create_masked", "sched_proble
             "sched_problem_destroy",
             "sched_mapping_modes", "sched_mapping_index", "sched_num_tools",
             "sched_num_mappings", "sched_workspace_bytes", "sched_bruteforce_argmin",
-            "sched_bruteforce_record",
+            "sched_bruteforce_record", "sched_bruteforce_argmin_noalloc",
             "sched_eval_batch", "sched_eval_mappings", "sched_eval_reprobes",
             "sched_pruned_workspace_bytes", "sched_pruned_argmin",
             "sched_monitor_create", "sched_monitor_destroy", "sched_monitor_observe",
@@ -120,6 +120,9 @@ def lib():
         L.sched_bruteforce_argmin.restype = ctypes.c_int
         L.sched_bruteforce_argmin.argtypes = [P, ctypes.c_uint64, ctypes.c_uint64, P,
                                               ctypes.c_size_t, P, ctypes.POINTER(sched_result)]
+        L.sched_bruteforce_argmin_noalloc.restype = ctypes.c_int
+        L.sched_bruteforce_argmin_noalloc.argtypes = [P, ctypes.c_uint64, ctypes.c_uint64, P,
+                                                      ctypes.POINTER(sched_result)]
         L.sched_bruteforce_record.restype = ctypes.c_int
         L.sched_bruteforce_record.argtypes = [P, P, ctypes.c_size_t, P, P, ctypes.c_uint64,
                                               ctypes.POINTER(sched_result)]
@@ -273,6 +276,16 @@ def sched_bruteforce_argmin(handle, lo: int, hi: int, workspace, stream=None) ->
     wp, wb = _ws(workspace)
     _check(lib().sched_bruteforce_argmin(handle, lo, hi, wp, wb, _stream_ptr(stream),
                                          ctypes.byref(out)), "sched_bruteforce_argmin")
+    return out.best_index, out.makespan_us
+
+
+def sched_bruteforce_argmin_noalloc(handle, lo: int, hi: int, stream=None) -> Tuple[int, int]:
+    """(best_index, makespan_us) over [lo, hi) without a workspace (the
+    library's per-GPU array; calls overlapping on one GPU race)."""
+    out = sched_result()
+    _check(lib().sched_bruteforce_argmin_noalloc(handle, lo, hi, _stream_ptr(stream),
+                                                 ctypes.byref(out)),
+           "sched_bruteforce_argmin_noalloc")
     return out.best_index, out.makespan_us
 
 

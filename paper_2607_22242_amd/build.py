@@ -15,7 +15,8 @@ INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 # (source, extra flags); the kernel instantiations are split by tool count so
 # that they compile in parallel.
 INST_PARTS = [(1, 12), (13, 17), (18, 21), (22, 25), (26, 29), (30, 32), (33, 36), (37, 40)]
-UNITS = [("api.cpp", []), ("monitor.cpp", []), ("dispatch.hip", []), ("probe.hip", [])] + [
+UNITS = [("api.cpp", []), ("monitor.cpp", []), ("dispatch.hip", []), ("probe.hip", []),
+         ("scratch.hip", [])] + [
     ("inst.hip", [f"-DINST_LO={lo}", f"-DINST_HI={hi}"]) for lo, hi in INST_PARTS]
 ARCH = "gfx950"
 

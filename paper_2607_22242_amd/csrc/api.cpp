@@ -30,7 +30,8 @@ struct sched_problem {
   uint64_t n_mappings = 0;
   int32_t n_preds = 0;
   uint32_t table_words = 0;
-  std::vector<uint32_t> table;  // device image with the problem's own latencies
+  std::vector<uint32_t> table;       // device image with the problem's own latencies
+  std::vector<uint32_t> table_full;  // the same, ordered for a one-table full-range search
 };
 
 namespace {
@@ -243,15 +244,28 @@ bool prefix_plan(const sched_problem& p, uint64_t n_tables) {
   return (unsigned __int128)(p.n_mappings / inner) * n_tables >= kTargetLanes;
 }
 
-std::vector<int32_t> enumeration(const sched_problem& p, bool full, int J, bool prefix) {
-  if (!full) return p.enum_tools;
-  std::vector<int32_t> late;
+// A sequence of tools (an enumeration order) held without heap memory, so
+// that planning a search allocates nothing.
+struct Seq {
+  int32_t v[kMaxTools];
+  int n = 0;
+  void push_back(int32_t x) { v[n++] = x; }
+  int size() const { return n; }
+  int32_t operator[](int k) const { return v[k]; }
+};
+
+Seq enumeration(const sched_problem& p, bool full, int J, bool prefix) {
+  Seq seq;
+  if (!full) {
+    for (int32_t v : p.enum_tools) seq.push_back(v);
+    return seq;
+  }
+  Seq late;
   for (int32_t v : p.late)
     if (p.radix[v] > 1) late.push_back(v);
   if (prefix) return late;
-  const int P = int(late.size());
+  const int P = late.size();
   const int lanes = std::min(4, P - J);
-  std::vector<int32_t> seq;
   for (int k = 0; k < J; ++k) seq.push_back(late[lanes + k]);
   for (int k = 0; k < lanes; ++k) seq.push_back(late[k]);
   for (int k = lanes + J; k < P; ++k) seq.push_back(late[k]);
@@ -266,7 +280,7 @@ std::vector<uint8_t> plan_key(const sched_problem& p) {
   return k;
 }
 
-uint64_t inner_count(const sched_problem& p, const std::vector<int32_t>& seq, int J) {
+uint64_t inner_count(const sched_problem& p, const Seq& seq, int J) {
   uint64_t c = 1;
   for (int k = 0; k < J; ++k) c *= p.radix[seq[k]];
   return c;
@@ -309,15 +323,23 @@ void plan_search(const sched_problem& p, uint64_t lo, uint64_t hi, uint32_t n_ta
   a.lds_levels = table_levels(p);
 }
 
-// Write the enumeration order seq into a table built by build_table.
-void set_enumeration(const sched_problem& p, const std::vector<int32_t>& seq, uint32_t* table) {
-  for (size_t k = 0; k < seq.size(); ++k) {
+// Write the enumeration order seq[0..n) into a table built by build_table.
+void set_enumeration(const sched_problem& p, const int32_t* seq, int n, uint32_t* table) {
+  for (int k = 0; k < n; ++k) {
     const int v = seq[k];
     table[kEnumLabBase + k] = table[kPosBase + v];
     table[kEnumWeightBase + 2 * k] = uint32_t(p.weight[v]);
     table[kEnumWeightBase + 2 * k + 1] = uint32_t(p.weight[v] >> 32);
     table[kEnumOptBase + k] = options_word(p, v);
   }
+}
+
+void set_enumeration(const sched_problem& p, const Seq& seq, uint32_t* table) {
+  set_enumeration(p, seq.v, seq.n, table);
+}
+
+void set_enumeration(const sched_problem& p, const std::vector<int32_t>& seq, uint32_t* table) {
+  set_enumeration(p, seq.data(), int(seq.size()), table);
 }
 
 size_t partial_capacity(uint64_t n_tables) {
@@ -460,6 +482,12 @@ int create_problem(const sched_tool* tools, int32_t n_tools, const sched_edge* e
       delete p;
       return rc;
     }
+    // the table of a one-table full-range search, in its enumeration order
+    SearchArgs a{};
+    plan_search(*p, 0, p->n_mappings, 1, a);
+    p->table_full = p->table;
+    set_enumeration(*p, enumeration(*p, true, int(a.inner_digits), a.prefix != 0),
+                    p->table_full.data());
   } catch (const std::bad_alloc&) {
     delete p;
     return SCHED_E_NOMEM;
@@ -571,6 +599,37 @@ PruneLayout prune_layout(const sched_problem& p, const PrunePlan& pl) {
   return l;
 }
 
+// Workspace bytes of one search over one problem table.
+size_t one_search_bytes(const sched_problem& p) {
+  return layout_for(size_t(p.table_words) * 4, partial_capacity(1), 1).total;
+}
+
+// One search of [lo, hi) in workspace ws (at least one_search_bytes): table
+// copy, search and reduction on stream s, then the result.  record: every
+// mapping's makespan (full ranges only; null: none).  Allocates nothing.
+int search_one(const sched_problem& p, uint64_t lo, uint64_t hi, char* ws, hipStream_t s,
+               uint32_t* record, sched_result* h_out) {
+  const Layout L = layout_for(size_t(p.table_words) * 4, partial_capacity(1), 1);
+  SearchArgs a{};
+  plan_search(p, lo, hi, 1, a);
+  a.tables = reinterpret_cast<const uint32_t*>(ws + L.tables);
+  a.table_stride = p.table_words;
+  a.partials = reinterpret_cast<Partial*>(ws + L.partials);
+  a.record = record;
+  DevResult* d_res = reinterpret_cast<DevResult*>(ws + L.results);
+  const std::vector<uint32_t>& table = a.full_range ? p.table_full : p.table;
+  HIP_TRY(hipMemcpyAsync(ws + L.tables, table.data(), size_t(p.table_words) * 4,
+                         hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_search(p.n, a, s));
+  HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, 1, d_res, s));
+  DevResult r;
+  HIP_TRY(hipMemcpyAsync(&r, d_res, sizeof(r), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  h_out->best_index = r.index;
+  h_out->makespan_us = r.makespan;
+  return SCHED_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -658,37 +717,21 @@ int sched_bruteforce_argmin(const sched_problem* p, uint64_t lo, uint64_t hi, vo
                             size_t ws_bytes, void* hip_stream, sched_result* h_out) {
   if (p == nullptr || h_out == nullptr) return SCHED_E_NULL;
   if (lo >= hi || hi > p->n_mappings) return SCHED_E_RANGE;
-  const Layout L = layout_for(size_t(p->table_words) * 4, partial_capacity(1), 1);
-  int rc = check_workspace(d_workspace, ws_bytes, L.total);
+  const int rc = check_workspace(d_workspace, ws_bytes, one_search_bytes(*p));
   if (rc != SCHED_OK) return rc;
-  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
-  char* ws = static_cast<char*>(d_workspace);
+  return search_one(*p, lo, hi, static_cast<char*>(d_workspace),
+                    reinterpret_cast<hipStream_t>(hip_stream), nullptr, h_out);
+}
 
-  SearchArgs a{};
-  plan_search(*p, lo, hi, 1, a);
-  a.tables = reinterpret_cast<const uint32_t*>(ws + L.tables);
-  a.table_stride = p->table_words;
-  a.partials = reinterpret_cast<Partial*>(ws + L.partials);
-  DevResult* d_res = reinterpret_cast<DevResult*>(ws + L.results);
-
-  std::vector<uint32_t> table;
-  try {
-    table = p->table;
-  } catch (const std::bad_alloc&) {
-    return SCHED_E_NOMEM;
-  }
-  if (a.full_range)
-    set_enumeration(*p, enumeration(*p, true, int(a.inner_digits), a.prefix != 0), table.data());
-  HIP_TRY(hipMemcpyAsync(ws + L.tables, table.data(), size_t(p->table_words) * 4,
-                         hipMemcpyHostToDevice, s));
-  HIP_TRY(launch_search(p->n, a, s));
-  HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, 1, d_res, s));
-  DevResult r;
-  HIP_TRY(hipMemcpyAsync(&r, d_res, sizeof(r), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
-  h_out->best_index = r.index;
-  h_out->makespan_us = r.makespan;
-  return SCHED_OK;
+int sched_bruteforce_argmin_noalloc(const sched_problem* p, uint64_t lo, uint64_t hi,
+                                    void* hip_stream, sched_result* h_out) {
+  if (p == nullptr || h_out == nullptr) return SCHED_E_NULL;
+  if (lo >= hi || hi > p->n_mappings) return SCHED_E_RANGE;
+  if (one_search_bytes(*p) > kScratchBytes) return SCHED_E_WORKSPACE;
+  void* ws = nullptr;
+  HIP_TRY(scratch_buffer(&ws));
+  return search_one(*p, lo, hi, static_cast<char*>(ws), reinterpret_cast<hipStream_t>(hip_stream),
+                    nullptr, h_out);
 }
 
 int sched_bruteforce_record(const sched_problem* p, void* d_workspace, size_t ws_bytes,
@@ -696,37 +739,10 @@ int sched_bruteforce_record(const sched_problem* p, void* d_workspace, size_t ws
                             sched_result* h_out) {
   if (p == nullptr || h_out == nullptr || d_makespan == nullptr) return SCHED_E_NULL;
   if (capacity < p->n_mappings) return SCHED_E_WORKSPACE;
-  const Layout L = layout_for(size_t(p->table_words) * 4, partial_capacity(1), 1);
-  int rc = check_workspace(d_workspace, ws_bytes, L.total);
+  const int rc = check_workspace(d_workspace, ws_bytes, one_search_bytes(*p));
   if (rc != SCHED_OK) return rc;
-  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
-  char* ws = static_cast<char*>(d_workspace);
-
-  SearchArgs a{};
-  plan_search(*p, 0, p->n_mappings, 1, a);
-  a.tables = reinterpret_cast<const uint32_t*>(ws + L.tables);
-  a.table_stride = p->table_words;
-  a.partials = reinterpret_cast<Partial*>(ws + L.partials);
-  a.record = d_makespan;
-  DevResult* d_res = reinterpret_cast<DevResult*>(ws + L.results);
-
-  std::vector<uint32_t> table;
-  try {
-    table = p->table;
-  } catch (const std::bad_alloc&) {
-    return SCHED_E_NOMEM;
-  }
-  set_enumeration(*p, enumeration(*p, true, int(a.inner_digits), a.prefix != 0), table.data());
-  HIP_TRY(hipMemcpyAsync(ws + L.tables, table.data(), size_t(p->table_words) * 4,
-                         hipMemcpyHostToDevice, s));
-  HIP_TRY(launch_search(p->n, a, s));
-  HIP_TRY(launch_reduce(a.partials, a.blocks_per_table, 1, d_res, s));
-  DevResult r;
-  HIP_TRY(hipMemcpyAsync(&r, d_res, sizeof(r), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
-  h_out->best_index = r.index;
-  h_out->makespan_us = r.makespan;
-  return SCHED_OK;
+  return search_one(*p, 0, p->n_mappings, static_cast<char*>(d_workspace),
+                    reinterpret_cast<hipStream_t>(hip_stream), d_makespan, h_out);
 }
 
 int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,

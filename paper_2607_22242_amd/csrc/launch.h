@@ -13,6 +13,10 @@ hipError_t launch_bound(int n_tools, const uint32_t* tab, uint32_t K, uint64_t k
                         uint32_t ub, uint32_t* count, uint2* out, hipStream_t s);
 hipError_t launch_reduce(const Partial* partials, uint32_t per_table, uint32_t n_tables,
                          DevResult* out, hipStream_t s);
+// Bytes of the per-GPU scratch array of the entry point that allocates
+// nothing: one problem table, 65,536 block partials and a result fit.
+constexpr size_t kScratchBytes = size_t(2) << 20;
+hipError_t scratch_buffer(void** ptr);
 hipError_t launch_valu_probe(uint32_t blocks, uint32_t iters, uint32_t* out, hipStream_t s,
                              double* lane_ops);
 
