@@ -201,14 +201,23 @@ int sched_eval_batch(const sched_problem *const *problems, int32_t n_problems,
                      int32_t n_replicas, void *d_workspace, size_t ws_bytes,
                      void *hip_stream, sched_result *h_out);
 
-/* Score explicit mappings (the what-if probes of Section 3.2): d_idx and
- * d_makespan are device arrays of n entries; each index must be below the
- * number of mappings.
- * d_makespan[i] receives the makespan of d_idx[i] in us, or INT64_MAX when
- * that mapping is infeasible.  Out-of-range indices also yield INT64_MAX. */
-int sched_eval_mappings(const sched_problem *p, const uint64_t *d_idx, int64_t n,
-                        int64_t *d_makespan, void *d_workspace, size_t ws_bytes,
-                        void *hip_stream);
+/* Score explicit mappings (the what-if probes of Section 3.2): h_idx is a
+ * host array of n indices, each below the number of mappings (else
+ * SCHED_E_RANGE, checked before any device work); h_makespan (host, n
+ * entries) receives each mapping's makespan in us, or INT64_MAX when it is
+ * infeasible.  The library copies the indices through d_workspace in chunks
+ * (at least one index beyond the problem table must fit; the bytes of
+ * sched_workspace_bytes take 65,536 per chunk) and waits for the stream. */
+int sched_eval_mappings(const sched_problem *p, const uint64_t *h_idx, int64_t n,
+                        void *d_workspace, size_t ws_bytes, void *hip_stream,
+                        int64_t *h_makespan);
+
+/* The same on device arrays (no host copies): d_idx and d_makespan hold n
+ * entries each; an index beyond the number of mappings yields INT64_MAX.  The
+ * workspace holds the problem table only. */
+int sched_eval_mappings_device(const sched_problem *p, const uint64_t *d_idx, int64_t n,
+                               int64_t *d_makespan, void *d_workspace, size_t ws_bytes,
+                               void *hip_stream);
 
 /* One what-if probe around a base mapping. */
 typedef struct {

@@ -28,7 +28,8 @@ EXPORTED = ["sched_problem_create", "sched_problem_create_masked", "sched_proble
             "sched_mapping_modes", "sched_mapping_index", "sched_num_tools",
             "sched_num_mappings", "sched_workspace_bytes", "sched_bruteforce_argmin",
             "sched_bruteforce_record", "sched_bruteforce_argmin_noalloc",
-            "sched_eval_batch", "sched_eval_mappings", "sched_eval_reprobes",
+            "sched_eval_batch", "sched_eval_mappings", "sched_eval_mappings_device",
+            "sched_eval_reprobes",
             "sched_pruned_workspace_bytes", "sched_pruned_argmin",
             "sched_monitor_create", "sched_monitor_destroy", "sched_monitor_observe",
             "sched_monitor_averages", "sched_monitor_latencies", "sched_valu_probe",
@@ -130,7 +131,9 @@ def lib():
         L.sched_eval_batch.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32, P,
                                        ctypes.c_size_t, P, P]
         L.sched_eval_mappings.restype = ctypes.c_int
-        L.sched_eval_mappings.argtypes = [P, P, ctypes.c_int64, P, P, ctypes.c_size_t, P]
+        L.sched_eval_mappings.argtypes = [P, P, ctypes.c_int64, P, ctypes.c_size_t, P, P]
+        L.sched_eval_mappings_device.restype = ctypes.c_int
+        L.sched_eval_mappings_device.argtypes = [P, P, ctypes.c_int64, P, P, ctypes.c_size_t, P]
         L.sched_eval_reprobes.restype = ctypes.c_int
         L.sched_eval_reprobes.argtypes = [P, ctypes.c_uint64, P, P, ctypes.c_size_t, P, P,
                                           ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
@@ -318,15 +321,29 @@ def sched_eval_batch(handles: Sequence, replica_problem: Sequence[int],
     return [(out[i].best_index, out[i].makespan_us) for i in range(R)]
 
 
-def sched_eval_mappings(handle, d_idx, d_makespan, workspace, stream=None) -> None:
+def sched_eval_mappings(handle, idx, workspace, stream=None):
+    """Makespans (int64 numpy array, INT64_MAX = infeasible) of the mapping
+    indices idx (host sequence or array); the library copies them through
+    the workspace."""
+    import numpy as np
+    a = np.ascontiguousarray(np.asarray(idx, dtype=np.uint64))
+    out = np.empty(len(a), dtype=np.int64)
+    wp, wb = _ws(workspace)
+    _check(lib().sched_eval_mappings(handle, a.ctypes.data, len(a), wp, wb, _stream_ptr(stream),
+                                     out.ctypes.data), "sched_eval_mappings")
+    return out
+
+
+def sched_eval_mappings_device(handle, d_idx, d_makespan, workspace, stream=None) -> None:
     """Score the device indices d_idx (int64 or uint64 tensor) into the
     int64 device tensor d_makespan (INT64_MAX = infeasible)."""
     n = d_idx.numel()
     assert d_makespan.numel() == n and d_idx.element_size() == 8
     assert d_idx.is_contiguous() and d_makespan.is_contiguous()
     wp, wb = _ws(workspace)
-    _check(lib().sched_eval_mappings(handle, d_idx.data_ptr(), n, d_makespan.data_ptr(), wp, wb,
-                                     _stream_ptr(stream)), "sched_eval_mappings")
+    _check(lib().sched_eval_mappings_device(handle, d_idx.data_ptr(), n, d_makespan.data_ptr(),
+                                            wp, wb, _stream_ptr(stream)),
+           "sched_eval_mappings_device")
 
 
 def sched_valu_probe(blocks: int, iters: int, d_out, stream=None) -> float:

@@ -181,7 +181,12 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
   }
   for (int l = 0; l < levels; ++l) {
     const uint64_t f = p.contention[l];
-    out[share_off + 2 * uint32_t(n) + uint32_t(l)] = uint32_t(((1ull << 33) + f) / (2 * f));
+    const uint64_t w = ((1ull << 33) + f) / (2 * f);
+    out[share_off + 2 * uint32_t(n) + uint32_t(l)] = uint32_t(w);
+    // floor(2^48 / w): the device divides by w through this reciprocal
+    const uint64_t winv = (1ull << 48) / w;
+    out[share_off + 2 * uint32_t(n) + uint32_t(levels) + 2 * uint32_t(l)] = uint32_t(winv);
+    out[share_off + 2 * uint32_t(n) + uint32_t(levels) + 2 * uint32_t(l) + 1] = uint32_t(winv >> 32);
   }
   out[kHdrShareOff] = share_off;
   // Bound table: shortest durations per mode and over the allowed modes.
@@ -849,9 +854,9 @@ int sched_eval_batch(const sched_problem* const* problems, int32_t n_problems,
   return SCHED_OK;
 }
 
-int sched_eval_mappings(const sched_problem* p, const uint64_t* d_idx, int64_t n,
-                        int64_t* d_makespan, void* d_workspace, size_t ws_bytes,
-                        void* hip_stream) {
+int sched_eval_mappings_device(const sched_problem* p, const uint64_t* d_idx, int64_t n,
+                               int64_t* d_makespan, void* d_workspace, size_t ws_bytes,
+                               void* hip_stream) {
   if (p == nullptr) return SCHED_E_NULL;
   if (n < 0) return SCHED_E_SIZE;
   if (n == 0) return SCHED_OK;
@@ -864,6 +869,39 @@ int sched_eval_mappings(const sched_problem* p, const uint64_t* d_idx, int64_t n
                          hipMemcpyHostToDevice, s));
   HIP_TRY(launch_eval(p->n, static_cast<const uint32_t*>(d_workspace), d_idx, n, p->n_mappings,
                       d_makespan, uint32_t(p->sharing), s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return SCHED_OK;
+}
+
+int sched_eval_mappings(const sched_problem* p, const uint64_t* h_idx, int64_t n,
+                        void* d_workspace, size_t ws_bytes, void* hip_stream,
+                        int64_t* h_makespan) {
+  if (p == nullptr) return SCHED_E_NULL;
+  if (n < 0) return SCHED_E_SIZE;
+  if (n == 0) return SCHED_OK;
+  if (h_idx == nullptr || h_makespan == nullptr) return SCHED_E_NULL;
+  for (int64_t i = 0; i < n; ++i)
+    if (h_idx[i] >= p->n_mappings) return SCHED_E_RANGE;
+  // the table, then chunks of indices and makespans (8 bytes each) in the
+  // rest of the workspace
+  const size_t head = align_up(size_t(p->table_words) * 4);
+  int rc = check_workspace(d_workspace, ws_bytes, head + kAlign + 16);
+  if (rc != SCHED_OK) return rc;
+  // chunk indices, then chunk makespans at the next 256-byte boundary: fits
+  const int64_t chunk = int64_t(std::min<size_t>((ws_bytes - head - kAlign) / 16, size_t(1) << 24));
+  char* ws = static_cast<char*>(d_workspace);
+  uint64_t* d_idx = reinterpret_cast<uint64_t*>(ws + head);
+  int64_t* d_out = reinterpret_cast<int64_t*>(ws + head + align_up(size_t(chunk) * 8));
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  HIP_TRY(hipMemcpyAsync(ws, p->table.data(), size_t(p->table_words) * 4,
+                         hipMemcpyHostToDevice, s));
+  for (int64_t at = 0; at < n; at += chunk) {
+    const int64_t m = std::min(chunk, n - at);
+    HIP_TRY(hipMemcpyAsync(d_idx, h_idx + at, size_t(m) * 8, hipMemcpyHostToDevice, s));
+    HIP_TRY(launch_eval(p->n, reinterpret_cast<const uint32_t*>(ws), d_idx, m, p->n_mappings,
+                        d_out, uint32_t(p->sharing), s));
+    HIP_TRY(hipMemcpyAsync(h_makespan + at, d_out, size_t(m) * 8, hipMemcpyDeviceToHost, s));
+  }
   HIP_TRY(hipStreamSynchronize(s));
   return SCHED_OK;
 }

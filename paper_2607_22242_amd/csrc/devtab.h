@@ -93,12 +93,13 @@ constexpr uint32_t kBoundWords = 4;
 
 // Processor-sharing table (after the bound table): for internal label i,
 // b[2i] = gpu_us and b[2i + 1] = gpu_us + load_us (isolated latencies), then
-// for each contention level the work rate round(2^32 / F) in 2^-16 us of
-// isolated work per us.
+// for each contention level the work rate w = round(2^32 / F) in 2^-16 us of
+// isolated work per us, then for each level floor(2^48 / w) (two words, low
+// first), the reciprocal the device divides by.
 inline uint32_t table_words(int n, int n_preds, int levels) {
   uint32_t dur_off = kPredBase + ((uint32_t(n_preds) + 3u) & ~3u);
   return dur_off + uint32_t(n) * 2u * uint32_t(levels) + kBoundWords * uint32_t(n) +
-         2u * uint32_t(n) + uint32_t(levels);
+         2u * uint32_t(n) + 3u * uint32_t(levels);
 }
 
 struct Partial {

@@ -18,6 +18,7 @@
 
 #include "devtab.h"
 #include "launch.h"
+#include "reduce.h"
 
 namespace devmap {
 
@@ -485,19 +486,28 @@ __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict
   return ms;
 }
 
-// ceil(a / w) for a < 2^53 and 1 <= w < 2^17, exactly: a double estimate of
-// the quotient (off by at most one) corrected with integer remainders.
-__host__ __device__ __forceinline__ uint64_t ceil_div_small(uint64_t a, uint32_t w) {
-  uint64_t q = uint64_t(double(a) / double(w));
-  int64_t r = int64_t(a) - int64_t(q * uint64_t(w));
-  if (r < 0) {
-    q -= 1;
-    r += int64_t(w);
-  } else if (r >= int64_t(w)) {
+// High 64 bits of the 128-bit product x * y.
+__host__ __device__ __forceinline__ uint64_t mulhi64(uint64_t x, uint64_t y) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __umul64hi(x, y);
+#else
+  return uint64_t((unsigned __int128)x * y >> 64);
+#endif
+}
+
+// ceil(a / w) for a < 2^46 and 256 <= w <= 2^16, in integers only, with
+// winv = floor(2^48 / w) from the table: a * winv / 2^48 lies within a
+// quarter below a / w, so its floor is the quotient or one less, and one
+// remainder step makes it exact.
+__host__ __device__ __forceinline__ uint64_t ceil_div_small(uint64_t a, uint32_t w,
+                                                           uint64_t winv) {
+  uint64_t q = mulhi64(a << 16, winv);
+  uint64_t r = a - q * w;
+  if (r >= w) {
     q += 1;
-    r -= int64_t(w);
+    r -= w;
   }
-  return q + (r > 0 ? 1u : 0u);
+  return q + (r != 0 ? 1u : 0u);
 }
 
 // Event loop under processor sharing, one event time per call of step().
@@ -675,8 +685,11 @@ struct SimPS {
     }
     uint32_t w = 0;
     if (k) {
-      w = sh[2 * N + (k < levels ? k : levels) - 1];
-      next = umin32(next, t + uint32_t(ceil_div_small(vmin - V, w)));
+      const uint32_t lv = (k < levels ? k : levels) - 1;
+      w = sh[2 * N + lv];
+      const uint64_t winv = uint64_t(sh[2 * N + levels + 2 * lv]) |
+                            (uint64_t(sh[2 * N + levels + 2 * lv + 1]) << 32);
+      next = umin32(next, t + uint32_t(ceil_div_small(vmin - V, w, winv)));
     }
     if (next == kInf) return true;  // a queued task never fits
     V += uint64_t(next - t) * w;
@@ -699,34 +712,6 @@ __host__ __device__ __forceinline__ uint32_t evaluate_sharing(const uint32_t* __
   for (int pass = 0; pass < 4 * N + 4; ++pass)
     if (sim.step(tab, lds, levels, budget, pass, slot, ms)) break;
   return ms;
-}
-
-__device__ __forceinline__ void lex_min(uint32_t& ms, uint64_t& x, uint32_t oms, uint64_t ox) {
-  if (oms < ms || (oms == ms && ox < x)) {
-    ms = oms;
-    x = ox;
-  }
-}
-
-// Block-wide lexicographic min of (makespan, index); result valid in thread 0.
-__device__ __forceinline__ void block_min(uint32_t& ms, uint64_t& x) {
-  __shared__ uint32_t s_ms[kBlock / 64];
-  __shared__ uint64_t s_x[kBlock / 64];
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint32_t oms = __shfl_xor(ms, off);
-    const uint64_t ox = __shfl_xor(x, off);
-    lex_min(ms, x, oms, ox);
-  }
-  const int wave = threadIdx.x / 64;
-  if ((threadIdx.x & 63) == 0) {
-    s_ms[wave] = ms;
-    s_x[wave] = x;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int w = 1; w < kBlock / 64; ++w) lex_min(ms, x, s_ms[w], s_x[w]);
-  }
 }
 
 // Words [first, first + stride, ...) of the LDS image of table tab.  The

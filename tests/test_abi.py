@@ -92,6 +92,10 @@ def test_workspace_and_range_validation_before_any_device_work():
     assert err(r, 0, 3 ** 8, FakeWs(0, nbytes)) == "SCHED_E_WORKSPACE"
     assert err(r, 0, 3 ** 8, FakeWs(128, nbytes)) == "SCHED_E_WORKSPACE"
     assert err(r, 0, 3 ** 8, FakeWs(256, nbytes - 256)) == "SCHED_E_WORKSPACE"
+    ev = lambda idx, ws: S.sched_eval_mappings(P.handle, idx, ws, fs)  # noqa: E731
+    assert err(ev, [0, 3 ** 8], FakeWs(256, nbytes)) == "SCHED_E_RANGE"
+    assert err(ev, [0, 1], FakeWs(128, nbytes)) == "SCHED_E_WORKSPACE"
+    assert err(ev, [0, 1], FakeWs(256, 256)) == "SCHED_E_WORKSPACE"
     na = lambda lo, hi: S.sched_bruteforce_argmin_noalloc(P.handle, lo, hi, fs)  # noqa: E731
     assert err(na, 5, 5) == "SCHED_E_RANGE"
     assert err(na, 0, 3 ** 8 + 1) == "SCHED_E_RANGE"

@@ -48,7 +48,7 @@ def gpu_eval(torch, P, idx):
     d_idx = torch.from_numpy(idx.view(np.int64)).to("cuda")
     d_out = torch.empty(len(idx), dtype=torch.int64, device="cuda")
     ws = S.workspace([P.handle])
-    S.sched_eval_mappings(P.handle, d_idx, d_out, ws)
+    S.sched_eval_mappings_device(P.handle, d_idx, d_out, ws)
     return d_out.cpu().numpy()
 
 
@@ -88,6 +88,24 @@ def test_out_of_range_indices_are_infeasible(torch_cuda, O):
     say("eval_mappings out-of-range indices")
     got = gpu_eval(torch_cuda, P, idx)
     assert list(got[:3]) == [INF64] * 3 and got[3] == Q.eval_index(7)
+
+
+@pytest.mark.parametrize("c", [1, 2, 3])
+def test_eval_mappings_host_arrays(torch_cuda, O, c):
+    """The host-array form (the library copies indices and makespans through
+    the workspace, here in chunks of 1,000) against the device form and the
+    oracle."""
+    P, Q = both(synth.load(c), O)
+    idx = np.random.default_rng(70 + c).integers(0, P.n_mappings, 20_000, dtype=np.uint64)
+    full = S.workspace([P.handle])
+    # the one-problem workspace is the table, 65,536 16-byte partials and a
+    # 256-byte result slot: keep the table and room for 1,000 indices
+    head = full.numel() - (1 << 20) - 256
+    small = full[:head + 256 + 16 * 1000]
+    say(f"eval_mappings host arrays, config {c}")
+    got = S.sched_eval_mappings(P.handle, idx, small)
+    np.testing.assert_array_equal(got, gpu_eval(torch_cuda, P, idx))
+    np.testing.assert_array_equal(got, Q.eval_many(idx))
 
 
 @pytest.mark.parametrize("seed", range(32))
