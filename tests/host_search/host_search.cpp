@@ -33,6 +33,7 @@ hipError_t launch_reduce(const Partial*, uint32_t, uint32_t, DevResult*, hipStre
 hipError_t launch_valu_probe(uint32_t, uint32_t, uint32_t*, hipStream_t, double*) {
   return hipErrorUnknown;
 }
+hipError_t scratch_buffer(void**) { return hipErrorUnknown; }
 }  // namespace devmap
 
 using namespace devmap;
@@ -131,6 +132,14 @@ int main(int argc, char** argv) {
     printf("error %d\n", rc);
     return 1;
   }
+#ifdef HOST_SEARCH_ONLY_N
+  // a build for one tool count (the sanitizer build, which is slow to compile)
+  if (n != HOST_SEARCH_ONLY_N) {
+    printf("error tools\n");
+    return 1;
+  }
+  run<HOST_SEARCH_ONLY_N>(p, table_path);
+#else
   switch (n) {
 #define HOST_SEARCH_CASE(K) \
   case K:                   \
@@ -143,6 +152,7 @@ int main(int argc, char** argv) {
       printf("error tools\n");
       return 1;
   }
+#endif
   sched_problem_destroy(p);
   return 0;
 }
