@@ -127,16 +127,27 @@ static int64_t gpu_duration(const or_problem *P, int v, int mode, int k) {
 /* Simulate one mapping.  mode[v] in {0,1,2}.  On success returns the makespan
  * and, when the pointers are non-null, each tool's start and finish time.
  * Returns OR_INFEASIBLE when the mapping is infeasible. */
-int64_t oracle_schedule(const or_problem *P, const int32_t *mode,
-                        int64_t *start_out, int64_t *finish_out) {
+/* Steps of one fixed-at-start schedule, counted for the work model of a
+ * sequential event-driven evaluation (tools whose ready time was computed,
+ * their in-edges, tools started); the counting changes no result. */
+typedef struct {
+    int64_t edges;   /* in-edges of the tools whose ready time was computed */
+    int64_t started; /* tools started before the schedule ended */
+} or_counts;
+
+static int64_t schedule_fs(const or_problem *P, const int32_t *mode, int64_t *start_out,
+                           int64_t *finish_out, or_counts *cnt) {
     const int n = P->n;
     int state[OR_MAXN];
     int64_t S[OR_MAXN], C[OR_MAXN], r[OR_MAXN];
-    int preds_done[OR_MAXN], starting[OR_MAXN];
+    int preds_done[OR_MAXN], starting[OR_MAXN], seen[OR_MAXN];
     int n_started = 0;
     int64_t t = 0;
 
-    for (int v = 0; v < n; v++) state[v] = WAITING;
+    for (int v = 0; v < n; v++) {
+        state[v] = WAITING;
+        seen[v] = 0;
+    }
 
     for (;;) {
         /* 1. release */
@@ -158,6 +169,10 @@ int64_t oracle_schedule(const or_problem *P, const int32_t *mode,
             }
             preds_done[v] = all;
             r[v] = rv;
+            if (all && !seen[v]) {
+                seen[v] = 1;
+                if (cnt) cnt->edges += P->npred[v];
+            }
         }
 
         /* 2. immediate starts (cpu and gpu_now never wait) */
@@ -201,6 +216,7 @@ int64_t oracle_schedule(const or_problem *P, const int32_t *mode,
             S[v] = t;
             C[v] = t + (mode[v] == OR_CPU ? P->cpu[v] : gpu_duration(P, v, mode[v], k));
             n_started++;
+            if (cnt) cnt->started++;
         }
         if (n_started == n) break;
 
@@ -221,6 +237,11 @@ int64_t oracle_schedule(const or_problem *P, const int32_t *mode,
         if (finish_out) finish_out[v] = C[v];
     }
     return makespan;
+}
+
+int64_t oracle_schedule(const or_problem *P, const int32_t *mode,
+                        int64_t *start_out, int64_t *finish_out) {
+    return schedule_fs(P, mode, start_out, finish_out, 0);
 }
 
 /* Work rate of a GPU task while k GPU tasks run: round(2^32 / F[k]) units of
@@ -363,6 +384,21 @@ int64_t oracle_eval_index(const or_problem *P, uint64_t x) {
     int32_t mode[OR_MAXN];
     decode_index(P->n, x, mode);
     return oracle_simulate(P, mode, 0, 0);
+}
+
+/* Summed step counts of the fixed-at-start schedules of mappings idx[0..count):
+ * out[0] in-edges of tools whose ready time was computed, out[1] tools
+ * started, out[2] feasible mappings. */
+void oracle_count_steps(const or_problem *P, const uint64_t *idx, int64_t count, int64_t *out) {
+    out[0] = out[1] = out[2] = 0;
+    for (int64_t i = 0; i < count; i++) {
+        int32_t mode[OR_MAXN];
+        decode_index(P->n, idx[i], mode);
+        or_counts c = {0, 0};
+        if (schedule_fs(P, mode, 0, 0, &c) != OR_INFEASIBLE) out[2]++;
+        out[0] += c.edges;
+        out[1] += c.started;
+    }
 }
 
 uint64_t oracle_num_mappings(const or_problem *P) {

@@ -62,6 +62,9 @@ def lib():
         L.oracle_argmin.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
                                     ctypes.c_int32, ctypes.POINTER(ctypes.c_uint64),
                                     ctypes.POINTER(ctypes.c_int64)]
+        L.oracle_count_steps.restype = None
+        L.oracle_count_steps.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                         ctypes.c_void_p]
         L.oracle_eval_many.restype = None
         L.oracle_eval_many.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                        ctypes.c_int32, ctypes.c_void_p]
@@ -128,6 +131,15 @@ class Problem:
         lib().oracle_eval_many(self.ptr, a.ctypes.data, len(a),
                                threads or default_threads(), out.ctypes.data)
         return out
+
+    def count_steps(self, idx) -> Tuple[int, int, int]:
+        """Summed over the fixed-at-start schedules of base-3 indices idx:
+        (in-edges of tools whose ready time was computed, tools started,
+        feasible mappings)."""
+        a = np.ascontiguousarray(np.asarray(idx, dtype=np.uint64))
+        out = np.zeros(3, dtype=np.int64)
+        lib().oracle_count_steps(self.ptr, a.ctypes.data, len(a), out.ctypes.data)
+        return int(out[0]), int(out[1]), int(out[2])
 
     def argmin(self, lo: int = 0, hi: Optional[int] = None,
                threads: Optional[int] = None) -> Tuple[int, int]:

@@ -800,3 +800,27 @@ def test_relabelling_tools_preserves_makespans_without_queue(oracle_mod):
         for v in range(n):
             m2[perm[v]] = modes[v]
         assert P1.schedule(list(modes))[0] == P2.schedule(m2)[0]
+
+
+def test_step_counts_of_the_work_model(oracle_mod):
+    """The oracle's step counts behind the per-mapping work figure
+    (tests/golden/count_ops.py): a chain where every mapping is feasible
+    reads every edge and starts every tool; an out-of-memory start ends the
+    count there.  Hand-built: A and B sources, C after A; footprints 10, 95,
+    10 against a budget of 100; B runs long on the GPU."""
+    O = oracle_mod
+    inst = synth.load(0)
+    Q = O.Problem.from_instance(inst)
+    e, s, f = Q.count_steps(range(3 ** 8))
+    assert (e, s, f) == (7 * 3 ** 8, 8 * 3 ** 8, 3 ** 8)
+    tools = [[10, 20, 0, 5, 10], [1000, 2000, 0, 0, 95], [10, 20, 0, 3, 10]]
+    P = mk(O, tools, [[0, 2]], 100)
+    idx = lambda a, b, c: a + 3 * b + 9 * c  # noqa: E731
+    # A and B on gpu_now together: 105 > 100 at t = 0, nothing starts
+    assert P.count_steps([idx(1, 1, 0)]) == (0, 0, 0)
+    # A on the CPU, B on gpu_now: both start at 0; C becomes ready at
+    # 20 + 3 and runs out of VRAM beside B (95 + 10): one edge read, two starts
+    assert P.eval_index(idx(0, 1, 1)) == O.INFEASIBLE
+    assert P.count_steps([idx(0, 1, 1)]) == (1, 2, 0)
+    # the same with C on the CPU: feasible, everything counted
+    assert P.count_steps([idx(0, 1, 0)]) == (1, 3, 1)

@@ -1,5 +1,6 @@
 """The seeded instance generator and the committed instance files."""
 import json
+import os
 
 import pytest
 
@@ -105,3 +106,24 @@ def test_expected_file_matches_instances():
     for key, entry in exp.items():
         c = int(key[len("config"):])
         assert entry["instance_sha256"] == synth.sha256_of(c)
+
+
+def test_counted_work_per_mapping():
+    """tests/golden/ops_per_mapping.json (tests/golden/count_ops.py, oracle
+    only): where every mapping is feasible the count equals the work of a
+    complete evaluation; elsewhere it lies below it."""
+    import math
+    with open(os.path.join(os.path.dirname(__file__), "golden", "ops_per_mapping.json")) as f:
+        ops = json.load(f)
+
+    def complete(inst):
+        n, e = len(inst["tools"]), len(inst["edges"])
+        return n * (3.0 * e / n + 14.0 + 2.0 * math.log2(n)) + 6.0
+
+    for c in (0, 5):
+        assert ops[f"config{c}"]["feasible_fraction"] == 1.0
+        assert abs(ops[f"config{c}"]["ops_per_mapping"] - complete(synth.load(c))) < 1e-9
+    for c in (1, 2, 3):
+        rec = ops[f"config{c}"]
+        assert 0.3 < rec["feasible_fraction"] < 1.0
+        assert 6.0 < rec["ops_per_mapping"] < complete(synth.load(c))
