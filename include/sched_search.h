@@ -252,6 +252,8 @@ typedef struct {
     int64_t initial_bound_us;   /* makespan of the descent's mapping (INT64_MAX if none) */
     int32_t prefix_tools;       /* tools in the prefix (0: one exhaustive search) */
     int32_t descent_rounds;     /* neighbourhood evaluations of the descent */
+    int32_t launches;           /* exhaustive-search launches */
+    int32_t shared_prefix_launches; /* of those, launches on the shared-prefix plan */
 } sched_prune_stats;
 
 /* Exact search with pruning: the same result as sched_bruteforce_argmin over

@@ -72,7 +72,8 @@ class sched_problem_desc(ctypes.Structure):
 class sched_prune_stats(ctypes.Structure):
     _fields_ = [("prefixes", ctypes.c_uint64), ("prefixes_searched", ctypes.c_uint64),
                 ("mappings_searched", ctypes.c_uint64), ("initial_bound_us", ctypes.c_int64),
-                ("prefix_tools", ctypes.c_int32), ("descent_rounds", ctypes.c_int32)]
+                ("prefix_tools", ctypes.c_int32), ("descent_rounds", ctypes.c_int32),
+                ("launches", ctypes.c_int32), ("shared_prefix_launches", ctypes.c_int32)]
 
 
 class SchedError(RuntimeError):

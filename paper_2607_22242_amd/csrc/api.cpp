@@ -27,6 +27,7 @@ struct sched_problem {
   std::vector<int32_t> enum_tools;          // tools with radix > 1, ascending
   int64_t budget = 0;
   int32_t sharing = 0;                      // 1: processor-sharing contention
+  bool free_fanout = false;                 // no edges, all footprints fit (kFlagFreeFanout)
   uint64_t n_mappings = 0;
   int32_t n_preds = 0;
   uint32_t table_words = 0;
@@ -214,6 +215,7 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
     out[bound_off + kBoundWords * uint32_t(i) + 3] = any;
   }
   out[kHdrBoundOff] = bound_off;
+  out[kHdrFlags] = p.free_fanout ? kFlagFreeFanout : 0u;
   return SCHED_OK;
 }
 
@@ -237,6 +239,7 @@ uint32_t table_levels(const sched_problem& p) {
 bool prefix_plan(const sched_problem& p, uint64_t n_tables) {
   if (p.n > (p.sharing ? kPrefixMaxNShare : kPrefixMaxN) || p.enum_tools.size() < kSharedInner)
     return false;
+  if (p.free_fanout) return false;  // scored in closed form, nothing to share
   // enough lanes left to fill the GPU with kSharedInner inner digits
   const std::vector<int32_t>& v = p.late;
   uint64_t inner = 1;
@@ -279,7 +282,7 @@ Seq enumeration(const sched_problem& p, bool full, int J, bool prefix) {
 
 // Replicas whose problems share this key share one search plan.
 std::vector<uint8_t> plan_key(const sched_problem& p) {
-  std::vector<uint8_t> k{uint8_t(p.n), uint8_t(p.sharing)};
+  std::vector<uint8_t> k{uint8_t(p.n), uint8_t(p.sharing), uint8_t(p.free_fanout)};
   for (int32_t v : p.late)
     if (p.radix[v] > 1) k.push_back(p.radix[v]);
   return k;
@@ -480,6 +483,11 @@ int create_problem(const sched_tool* tools, int32_t n_tools, const sched_edge* e
       if (p->radix[v] > 1) p->enum_tools.push_back(v);
     }
     p->n_mappings = w;
+    int64_t sum_mem = 0;
+    for (const sched_tool& t : p->tools) sum_mem += t.mem_mib;
+    bool identity = true;
+    for (int32_t i = 0; i < n_tools; ++i) identity = identity && p->order[i] == i;
+    p->free_fanout = total == 0 && sharing == 0 && p->budget >= sum_mem && identity;
     p->table_words = table_words(n_tools, total, std::min<int>(n_levels, n_tools));
     p->table.assign(p->table_words, 0u);
     const int rc = build_table(*p, nullptr, p->table.data());
@@ -993,6 +1001,8 @@ int sched_pruned_argmin(const sched_problem* p, void* d_workspace, size_t ws_byt
       st.prefixes = 1;
       st.prefixes_searched = 1;
       st.mappings_searched = p->n_mappings;
+      st.launches = 1;
+      st.shared_prefix_launches = prefix_plan(*p, 1) ? 1 : 0;
       st.initial_bound_us = INT64_MAX;
       *stats = st;
     }
@@ -1153,6 +1163,8 @@ int sched_pruned_argmin(const sched_problem* p, void* d_workspace, size_t ws_byt
         }
       st.prefixes_searched += count;
       st.mappings_searched += uint64_t(count) * sub.n_mappings;
+      st.launches += 1;
+      st.shared_prefix_launches += a.prefix ? 1 : 0;
       next = end;
     }
     h_out->best_index = best_ms == INT64_MAX ? ~0ull : best_x;

@@ -47,8 +47,16 @@ enum : uint32_t {
   kHdrBaseHi = 12,    // offset in the mapping index)
   kHdrBoundOff = 13,  // word offset of the bound table
   kHdrShareOff = 14,  // word offset of the processor-sharing table
+  kHdrFlags = 15,     // kFlag* bits
   kHdrWords = 16,
 };
+
+// A fan-out (no edges) whose footprints all fit the budget together, scored
+// with fixed-at-start contention: every tool is ready at 0, no start can run
+// out of memory and no queued tool waits for VRAM, so a mapping's schedule
+// follows in closed form (evaluate_fanout).  Its internal labels are the
+// original tool numbers.
+constexpr uint32_t kFlagFreeFanout = 1u;
 
 // Record of the tool with internal label i at kHdrWords + kToolWords * i.
 enum : uint32_t {

@@ -470,6 +470,71 @@ struct Sim {
   }
 };
 
+// Makespan of one mapping of a fan-out whose footprints all fit the budget
+// together (kFlagFreeFanout), fixed-at-start contention.  Every tool is ready
+// at 0.  The CPU tools end at their cpu_us.  The gpu_now tools and the first
+// queued tool (the lowest number: the queue orders ties by number) start at
+// 0 with k0 = #gpu_now + 1 co-running GPU tools (k0 = #gpu_now with an empty
+// queue), and the queue never waits for VRAM, so each later queued tool
+// starts when its predecessor in the queue ends, at s, beside the gpu_now
+// tools still running (finish > s: releases come first) and itself.  No other
+// event changes a duration.  Labels are tool numbers.  slot: the calling
+// wave's LDS word (see wave_or).
+template <int N>
+__host__ __device__ __forceinline__ uint32_t evaluate_fanout(const uint32_t* __restrict__ tab,
+                                                             const uint32_t* __restrict__ lds,
+                                                             uint32_t levels, MaskT<N> gnm,
+                                                             MaskT<N> gqm, MaskT<N>* slot) {
+  using M = MaskT<N>;
+  const uint32_t* s_dur = lds + lds_dur_off<N>();
+  constexpr uint32_t kRow = 2u * uint32_t(N);
+  const Tab tp = fresh(tab);
+  // tools some lane of the wave has on gpu_now / gpu_queue
+  M wn, wq, wx;
+  wave_or3<N>(gnm, gqm, M(0), slot, wn, wq, wx);
+  uint32_t k0;
+  if constexpr (N <= 32) {
+    k0 = uint32_t(__builtin_popcount(uint32_t(gnm)));
+  } else {
+    k0 = uint32_t(__builtin_popcountll(uint64_t(gnm)));
+  }
+  k0 += gqm != 0 ? 1u : 0u;
+  const uint32_t* row0 = s_dur + (umin32(umax32(k0, 1u), levels) - 1u) * kRow;
+  uint32_t f[N];  // finish of each gpu_now tool (0 for the others)
+  uint32_t mk = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    f[i] = 0;
+    if ((wn >> i) & 1) {
+      DEVMAP_KEEP_BRANCH();
+      if ((gnm >> i) & 1) f[i] = row0[2 * i];
+    }
+    const bool cpu = !(((gnm | gqm) >> i) & 1);
+    mk = umax32(mk, cpu ? opaque(tp[kHdrWords + kToolWords * i + kToolCpu]) : f[i]);
+  }
+  const M wn_q = opaque(wn), wq_q = opaque(wq);
+  uint32_t s = 0;  // when the queue frees
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    if ((wq_q >> i) & 1) {
+      DEVMAP_KEEP_BRANCH();
+      if ((gqm >> i) & 1) {
+        uint32_t k = 1;
+#pragma unroll
+        for (int v = 0; v < N; ++v) {
+          if ((wn_q >> v) & 1) {
+            DEVMAP_KEEP_BRANCH();
+            k += f[v] > s ? 1u : 0u;
+          }
+        }
+        s += s_dur[(umin32(k, levels) - 1u) * kRow + 2u * uint32_t(i) + 1u];
+        mk = umax32(mk, s);
+      }
+    }
+  }
+  return mk;
+}
+
 // Makespan of one mapping, or kInf if it is infeasible.  slot: the calling
 // wave's LDS word (see wave_or).
 template <int N>
@@ -478,6 +543,8 @@ __host__ __device__ __forceinline__ uint32_t evaluate(const uint32_t* __restrict
                                                       uint32_t levels, uint32_t budget,
                                                       MaskT<N> gnm, MaskT<N> gqm,
                                                       MaskT<N>* slot) {
+  if (Tab{tab}[kHdrFlags] & kFlagFreeFanout)
+    return evaluate_fanout<N>(tab, lds, levels, gnm, gqm, slot);
   Sim<N> sim;
   sim.init(tab, gnm, gqm);
   uint32_t ms = kInf;

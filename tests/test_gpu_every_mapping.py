@@ -81,6 +81,17 @@ def test_every_mapping_shared_prefix_plans(torch_cuda, O, shape, n, tight, seed)
     check_every(torch_cuda, P, Q.eval_many(np.arange(P.n_mappings, dtype=np.uint64)))
 
 
+@pytest.mark.parametrize("seed,n", [(8841, 14), (8842, 14), (8843, 9)])
+def test_every_mapping_fanout_without_vram_limit(torch_cuda, O, seed, n):
+    """Fan-outs whose footprints all fit the budget together (the fan-out
+    scenarios of the batch workload) are scored in closed form."""
+    inst = synth.random_instance(seed, n, "fanout")
+    inst["vram_budget_mib"] = sum(t[4] for t in inst["tools"]) + (seed % 2) * 1000
+    P, Q = S.Problem.from_instance(inst), O.Problem.from_instance(inst)
+    say(f"every mapping, free fan-out {n} tools, seed {seed}")
+    check_every(torch_cuda, P, Q.eval_many(np.arange(P.n_mappings, dtype=np.uint64)))
+
+
 @pytest.mark.parametrize("seed", [8821, 8822])
 def test_every_mapping_processor_sharing(torch_cuda, O, seed):
     """The processor-sharing evaluator on the shared-prefix plan (3^14)."""
