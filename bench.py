@@ -212,7 +212,9 @@ def main():
         problems = [S.Problem.from_instance(sc, sharing=args.sharing) for sc in scen]
         handles = [p.handle for p in problems]
         rp = [si for si, sc in enumerate(scen) for _ in sc["replicas"]]
-        lat = [rep for sc in scen for rep in sc["replicas"]]
+        import numpy as np
+        lat = np.array([row[:4] for sc in scen for rep in sc["replicas"] for row in rep],
+                       dtype=np.int64)
         ws = S.workspace(handles, len(rp))
         total = len(rp) * problems[0].n_mappings
         n_tools = problems[0].n

@@ -310,16 +310,26 @@ def sched_eval_batch(handles: Sequence, replica_problem: Sequence[int],
                      replica_lat: Sequence[Sequence[Sequence[int]]], workspace,
                      stream=None) -> List[Tuple[int, int]]:
     """Per-replica (best_index, makespan_us); replica_lat[r] holds N rows of
-    (gpu_us, cpu_us, load_us, xfer_us)."""
+    (gpu_us, cpu_us, load_us, xfer_us) (nested sequences, or an int64 array
+    whose rows are those of every replica in turn)."""
+    import numpy as np
     R = len(replica_problem)
-    rp = (ctypes.c_int32 * max(R, 1))(*map(int, replica_problem))
-    rows = [row for rep in replica_lat for row in rep]
-    lat = (sched_lat * max(len(rows), 1))(*[sched_lat(*map(int, r[:4])) for r in rows])
-    out = (sched_result * max(R, 1))()
+    rp = np.ascontiguousarray(np.asarray(replica_problem, dtype=np.int32).reshape(-1))
+    if isinstance(replica_lat, np.ndarray):
+        lat = np.ascontiguousarray(replica_lat[..., :4], dtype=np.int64).reshape(-1, 4)
+    else:
+        lat = np.ascontiguousarray(
+            np.asarray([row[:4] for rep in replica_lat for row in rep], dtype=np.int64)
+            .reshape(-1, 4))
+    if lat.size == 0:
+        lat = np.zeros((1, 4), dtype=np.int64)
+    out = np.zeros((max(R, 1), 2), dtype=np.int64)  # sched_result: uint64 index, int64 makespan
     wp, wb = _ws(workspace)
-    _check(lib().sched_eval_batch(_handles(handles), len(handles), rp, lat, R, wp, wb,
-                                  _stream_ptr(stream), out), "sched_eval_batch")
-    return [(out[i].best_index, out[i].makespan_us) for i in range(R)]
+    _check(lib().sched_eval_batch(_handles(handles), len(handles), rp.ctypes.data,
+                                  lat.ctypes.data, R, wp, wb,
+                                  _stream_ptr(stream), out.ctypes.data), "sched_eval_batch")
+    idx = out[:R, 0].view(np.uint64)
+    return [(int(idx[i]), int(out[i, 1])) for i in range(R)]
 
 
 def sched_eval_mappings(handle, idx, workspace, stream=None):
