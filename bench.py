@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 11785250000
-TRAFFIC_KERNEL_SHA256 = "7cd0621a56cbcda649583154974841d80c169fdb49cc724839357c4fc19daa31"
+TRAFFIC_BYTES = 12453510759
+TRAFFIC_KERNEL_SHA256 = "81434cd1aabd739528ea6d1f3d244aa91b9addfa7a954f7aee6ff38d4fd4d4b1"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 

@@ -67,9 +67,12 @@ enum : uint32_t {
   kToolPredHi = 4,    // predecessor mask bits 32..63
   kToolPredOff = 5,   // offset of the predecessor list (from kPredBase)
   kToolNPred = 6,     // number of predecessors
-  kToolOrig = 7,      // original tool number (queue ties go to the lowest)
+  kToolOrig = 7,      // (original tool number << 6) | label (queue ties go to the lowest number)
   kToolWords = 8,
 };
+
+constexpr uint32_t kOrigLabelMask = 63u;  // the label in the low bits of kToolOrig
+static_assert(kMaxTools <= 64, "labels must fit the low six bits of kToolOrig");
 
 // pos[v]: internal label of original tool v.
 constexpr uint32_t kPosBase = kHdrWords + kToolWords * kMaxTools;  // 336

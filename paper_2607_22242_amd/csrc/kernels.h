@@ -70,6 +70,26 @@ __host__ __device__ __forceinline__ M opaque(M x) {
 #endif
 
 __host__ __device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
+
+// c ? acc + x : acc (and c ? acc | x : acc) as an add (or) and one select.
+// The sum is formed first, opaque to the optimiser, so that a wave-uniform x
+// enters the add directly instead of being moved to a vector register for a
+// select of x or 0.
+__host__ __device__ __forceinline__ uint32_t add_if(uint32_t acc, uint32_t x, bool c) {
+  uint32_t s = acc + x;
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("" : "+v"(s));
+#endif
+  return c ? s : acc;
+}
+template <class M>
+__host__ __device__ __forceinline__ M or_if(M acc, M x, bool c) {
+  M s = acc | x;
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("" : "+v"(s));
+#endif
+  return c ? s : acc;
+}
 __host__ __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 
 template <int N>
@@ -91,8 +111,8 @@ __host__ __device__ __forceinline__ bool bit(MaskT<N> m, int v) {
 }
 
 // LDS image staged by every block: footprints by internal label, then the
-// internal label of every original tool, then the duration table (its
-// length follows the problem's contention levels), level-major:
+// duration table (its length follows the problem's contention levels),
+// level-major:
 // dur[(level - 1) * 2N + 2 * label + q] (q = 0 gpu_now, 1 gpu_queue), so a
 // pass finds its row once and each start reads one word at a fixed offset.
 template <int N>
@@ -100,12 +120,10 @@ constexpr uint32_t lds_levels() { return N < kMaxLevels ? N : kMaxLevels; }
 template <int N>
 constexpr uint32_t lds_mem_off() { return 0u; }
 template <int N>
-constexpr uint32_t lds_pos_off() { return uint32_t(N); }
-template <int N>
-constexpr uint32_t lds_dur_off() { return 2u * uint32_t(N); }
+constexpr uint32_t lds_dur_off() { return uint32_t(N); }
 // Words of the image for `levels` stored contention levels.
 __host__ __device__ constexpr uint32_t lds_words_for(int n, uint32_t levels) {
-  return 2u * uint32_t(n) + uint32_t(n) * 2u * levels;
+  return uint32_t(n) + uint32_t(n) * 2u * levels;
 }
 // The largest image a problem with N tools can need.
 template <int N>
@@ -268,7 +286,6 @@ struct Sim {
     const M gpum = gnm | gqm;
     const uint32_t* s_dur = lds + lds_dur_off<N>();
     const uint32_t* s_mem = lds + lds_mem_off<N>();
-    const uint32_t* s_pos = lds + lds_pos_off<N>();
     const Tab tp = fresh(tab);
     const uint32_t t1 = t + 1u;
     const uint32_t lim = kH - t1;  // d = x - t1 < lim: x is a time after t
@@ -289,8 +306,8 @@ struct Sim {
         const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
         const uint32_t d = T[i] - t1;
         const bool on = d < lim;  // finishes after t
-        in_use += on ? mem : 0u;
-        run |= on ? M(1) << i : M(0);
+        in_use = add_if(in_use, mem, on);
+        run = or_if(run, M(1) << i, on);
         tf = umin32(tf, d);
       }
     }
@@ -306,7 +323,7 @@ struct Sim {
         DEVMAP_KEEP_BRANCH();
         const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
         const bool on = T[i] == now_t;  // gpu_now, ready at t
-        in_use += on ? mem : 0u;
+        in_use = add_if(in_use, mem, on);
         k += on ? 1u : 0u;
       }
     }
@@ -314,6 +331,7 @@ struct Sim {
     uint32_t hsel = kInf;              // label of the queued tool admitted at t
     if (minq <= t && qfin <= t) {
       // the queue head: ready at minq (the earliest), lowest original number
+      // (the table's word holds the number above the label)
       const uint32_t key = kTagQueue + minq;
       uint32_t hO = kInf;
       const M ww_q = opaque(ww);
@@ -325,7 +343,7 @@ struct Sim {
           hO = T[i] == key ? umin32(hO, orig) : hO;
         }
       }
-      const uint32_t lab = s_pos[hO];
+      const uint32_t lab = hO & kOrigLabelMask;
       if (s_mem[lab] <= budget - in_use) {
         hsel = lab;
         k += 1;
@@ -795,7 +813,6 @@ __host__ __device__ __forceinline__ void stage_image(const uint32_t* tab, uint32
   }
   for (uint32_t i = first; i < uint32_t(N); i += stride) {
     lds[lds_mem_off<N>() + i] = tab[kHdrWords + kToolWords * i + kToolMem];
-    lds[lds_pos_off<N>() + i] = tab[kPosBase + i];
   }
 }
 
