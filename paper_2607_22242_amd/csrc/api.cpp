@@ -137,7 +137,7 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
     rec[kToolPredHi] = uint32_t(pm >> 32);
     rec[kToolPredOff] = pred_cursor;
     rec[kToolNPred] = uint32_t(pl.size());
-    rec[kToolOrig] = (uint32_t(v) << 6) | uint32_t(i);
+    rec[kToolOrig] = (uint32_t(v) << kOrigLabelBits) | uint32_t(i);
     for (int32_t u : pl) out[kPredBase + pred_cursor++] = uint32_t(u);
     out[kPosBase + v] = uint32_t(i);
     if (tl.mem_mib > budget) big |= 1ull << i;

@@ -67,12 +67,16 @@ enum : uint32_t {
   kToolPredHi = 4,    // predecessor mask bits 32..63
   kToolPredOff = 5,   // offset of the predecessor list (from kPredBase)
   kToolNPred = 6,     // number of predecessors
-  kToolOrig = 7,      // (original tool number << 6) | label (queue ties go to the lowest number)
+  kToolOrig = 7,      // (original tool number << kOrigLabelBits) | label
   kToolWords = 8,
 };
 
-constexpr uint32_t kOrigLabelMask = 63u;  // the label in the low bits of kToolOrig
-static_assert(kMaxTools <= 64, "labels must fit the low six bits of kToolOrig");
+// kToolOrig holds the original number above the label, so that the lowest
+// word among candidate tools names both the first in the queue's tie order and
+// its label.
+constexpr uint32_t kOrigLabelBits = 6;
+constexpr uint32_t kOrigLabelMask = (1u << kOrigLabelBits) - 1u;
+static_assert(kMaxTools <= (1 << kOrigLabelBits), "labels must fit below the original number");
 
 // pos[v]: internal label of original tool v.
 constexpr uint32_t kPosBase = kHdrWords + kToolWords * kMaxTools;  // 336

@@ -70,6 +70,7 @@ __host__ __device__ __forceinline__ M opaque(M x) {
 #endif
 
 __host__ __device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
+__host__ __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 
 // c ? acc + x : acc (and c ? acc | x : acc) as an add (or) and one select.
 // The sum is formed first, opaque to the optimiser, so that a wave-uniform x
@@ -90,7 +91,6 @@ __host__ __device__ __forceinline__ M or_if(M acc, M x, bool c) {
 #endif
   return c ? s : acc;
 }
-__host__ __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 
 template <int N>
 __host__ __device__ __forceinline__ MaskT<N> all_tools() {
