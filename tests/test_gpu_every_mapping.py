@@ -148,3 +148,33 @@ def test_every_mapping_mixed19_sampled(torch_cuda, O):
     np.testing.assert_array_equal(got, Q.eval_many(idx))
     del buf
     torch.cuda.empty_cache()
+
+
+def _random_mix(k):
+    """Case k of a seeded mix: shape, size, budget, contention levels, value
+    range and contention reading all drawn from k."""
+    rng = np.random.default_rng(7700 + k)
+    shape = ["random", "permuted", "chain", "fanout"][k % 4]
+    n = int(rng.integers(13, 16))
+    seed = int(rng.integers(1, 1 << 30))
+    tight = bool(rng.integers(0, 2))
+    small = bool(rng.integers(0, 4) == 0)
+    sharing = bool(rng.integers(0, 5) == 0) and n <= 14
+    levels = int(rng.choice([1, 2, 4, 7]))
+    inst = synth.random_instance(seed, n, shape, levels=levels, tight=tight, small_values=small)
+    if rng.integers(0, 3) == 0:
+        inst["vram_budget_mib"] = sum(t[4] for t in inst["tools"])
+    return inst, sharing
+
+
+@pytest.mark.parametrize("k", range(24))
+def test_every_mapping_random_mix(torch_cuda, O, k):
+    """24 seeded 3^13-3^15 problems mixing DAG shapes, budgets (a quarter of
+    the footprints, random, or all footprints together), 1 to 7 contention
+    levels, tie-heavy small latencies and both contention readings: every
+    mapping the search scores against the oracle."""
+    inst, sharing = _random_mix(k)
+    P = S.Problem.from_instance(inst, sharing=sharing)
+    Q = O.Problem.from_instance(inst, sharing=sharing)
+    say(f"every mapping, random mix {k}: {len(inst['tools'])} tools, sharing={sharing}")
+    check_every(torch_cuda, P, Q.eval_many(np.arange(P.n_mappings, dtype=np.uint64)))
