@@ -601,11 +601,16 @@ __host__ __device__ __forceinline__ uint64_t ceil_div_small(uint64_t a, uint32_t
 // but a GPU task's end is not fixed when it starts: every running GPU task
 // advances at the rate w_k of the k GPU tasks running, so with V the work
 // each has done since time 0, a task started at V_s with work b * 2^16 ends
-// when V reaches its virtual finish V_s + b * 2^16.  Each per-tool loop
-// visits a tool only where some lane of the wave has it running or waiting
-// (two wave-wide ORs per pass); elsewhere the tool is done everywhere and
-// its work would change nothing.  A tool's mode is first read in the pass
-// that finds all its predecessors done (readym).
+// when V reaches its virtual finish V_s + b * 2^16.  A CPU task neither
+// slows nor blocks anything and starts at its ready time, so it is resolved
+// (started, its end known) as soon as the ends of all its predecessors are
+// known, in one ascending sweep over the labels; its end is then no event.
+// A tool's ready time is computed once, when its predecessors' ends are all
+// known: a CPU predecessor's when it is resolved, a GPU predecessor's when it
+// is done.  Each per-tool loop visits a tool only where some lane of the wave
+// has it running or not yet started (two wave-wide ORs per pass); elsewhere
+// its work would change nothing.  A tool's mode is first read when its ready
+// time is computed (first_read: resolved | cpu).
 template <int N>
 struct SimPS {
   using M = MaskT<N>;
@@ -613,11 +618,13 @@ struct SimPS {
   // ready time while waiting and its end once started or done
   uint64_t Y[N];
   M gnm, gqm;
-  M running, done;
-  M readym;  // tools whose predecessors were all done at the last pass
+  M running, done;  // GPU tasks
+  M resolved;       // GPU tasks whose ready time is known
+  M cpu;            // CPU tasks, resolved: started at their ready time, end known
   uint64_t V;
   uint32_t t;
-  bool dead;  // statically infeasible
+  uint32_t mk;  // latest end of the CPU tasks
+  bool dead;    // statically infeasible
 
   __host__ __device__ __forceinline__ void init(const uint32_t* __restrict__ tab, M gn, M gq) {
     gnm = gn;
@@ -626,9 +633,11 @@ struct SimPS {
     for (int i = 0; i < N; ++i) Y[i] = 0;
     running = 0;
     done = 0;
-    readym = 0;
+    resolved = 0;
+    cpu = 0;
     V = 0;
     t = 0;
+    mk = 0;
     dead = ((gn | gq) & load_mask<N>(Tab{tab}, kHdrBigLo)) != 0;
   }
 
@@ -646,112 +655,104 @@ struct SimPS {
     const uint32_t* sh = tab + tab[kHdrShareOff];
     const M gpu = gnm | gqm;
     const M ALL = all_tools<N>();
-    // tools some lane of the wave has running / waiting
+    // tools some lane of the wave has running / not yet started
     M wr, ww;
     if constexpr (N <= 32) {
       const uint64_t both = wave_or<uint64_t>(
-          uint64_t(running) | (uint64_t(ALL & ~(running | done)) << 32),
+          uint64_t(running) | (uint64_t(ALL & ~(running | done | cpu)) << 32),
           reinterpret_cast<uint64_t*>(slot));
       wr = M(both);
       ww = M(both >> 32);
     } else {
       wr = wave_or<M>(running, slot);
-      ww = wave_or<M>(ALL & ~(running | done), slot);
+      ww = wave_or<M>(ALL & ~(running | done | cpu), slot);
     }
-    // 1. release: CPU tasks at their end, GPU tasks out of work
+    // 1. release: GPU tasks out of work; VRAM of those still running
+    uint32_t in_use = 0;
     const M wr1 = opaque(wr);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       if ((wr1 >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
-        const bool fin = ((running >> i) & 1) &&
-                         (((gpu >> i) & 1) ? Y[i] <= V : uint32_t(Y[i]) <= t);
+        const bool on = (running >> i) & 1;
+        const bool fin = on && Y[i] <= V;
         if (fin) {
           running &= ~(M(1) << i);
           done |= M(1) << i;
           Y[i] = t;
         }
+        const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
+        in_use = add_if(in_use, mem, on && !fin);
       }
     }
-    if (done == ALL) {
-      ms = t;
-      return true;
-    }
-    // 2. ready times of waiting tasks whose predecessors are done, and the
-    // immediate starts
-    const M waiting = ~(running | done) & ALL;
+    // 2. ready times of tasks whose predecessors' ends are all known (CPU
+    // tasks start there), and the immediate GPU starts
     M ready = 0, starting = 0;
-    uint32_t in_use = 0;
-    const M wr2 = opaque(wr);
-#pragma unroll
-    for (int i = 0; i < N; ++i)
-      if ((wr2 >> i) & 1) {
-        DEVMAP_KEEP_BRANCH();
-        if ((running >> i) & 1 && (gpu >> i) & 1) in_use += s_mem[i];
-      }
     const M ww2 = opaque(ww);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       if ((ww2 >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
-        const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
-        if ((waiting >> i) & 1 && (pm & ~done) == 0) {
-          const uint32_t xf = tp[kHdrWords + kToolWords * i + kToolXfer];
-          uint32_t r = 0;
+        const M bi = M(1) << i;
+        if (!((running | done | cpu | resolved) & bi)) {
+          const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
+          if ((pm & ~(done | cpu)) == 0) {
+            const uint32_t xf = tp[kHdrWords + kToolWords * i + kToolXfer];
+            uint32_t r = 0;
 #pragma unroll
-          for (int u = 0; u < i; ++u)
-            if ((pm >> u) & 1)
-              r = umax32(r, uint32_t(Y[u]) + ((((gpu >> u) ^ (gpu >> i)) & 1) ? xf : 0u));
-          Y[i] = r;
-          ready |= M(1) << i;
-          if (r <= t && !((gqm >> i) & 1)) {
-            starting |= M(1) << i;
-            if ((gnm >> i) & 1) in_use += s_mem[i];
+            for (int u = 0; u < i; ++u)
+              if ((pm >> u) & 1)
+                r = umax32(r, uint32_t(Y[u]) + ((((gpu >> u) ^ (gpu >> i)) & 1) ? xf : 0u));
+            if (gpu & bi) {
+              Y[i] = r;
+              resolved |= bi;
+            } else {
+              const uint32_t e = r + tp[kHdrWords + kToolWords * i + kToolCpu];
+              Y[i] = e;
+              cpu |= bi;
+              mk = umax32(mk, e);
+            }
+          }
+        }
+        if ((resolved & ~(running | done)) & bi) {
+          ready |= bi;
+          if (uint32_t(Y[i]) <= t && !((gqm >> i) & 1)) {
+            starting |= bi;
+            const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
+            in_use += mem;
           }
         }
       }
     }
+    if ((done | cpu) == ALL) {
+      ms = umax32(t, mk);
+      return true;
+    }
     if (in_use > budget) return true;  // out of memory: infeasible
     // 3. one queue admission when no queued task runs: FIFO on (ready, tool)
     if ((running & gqm) == 0) {
-      int head = -1;
-      uint32_t hr = kInf, ho = kInf;
+      // the lowest (ready time, original number), the label in the low bits
+      uint64_t hk = ~0ull;
       const M ww3 = opaque(ww);
 #pragma unroll
       for (int i = 0; i < N; ++i) {
         if ((ww3 >> i) & 1) {
           DEVMAP_KEEP_BRANCH();
           const uint32_t x = uint32_t(Y[i]);
-          if ((ready >> i) & 1 && (gqm >> i) & 1 && x <= t) {
-            const uint32_t o = tp[kHdrWords + kToolWords * i + kToolOrig];
-            if (x < hr || (x == hr && o < ho)) {
-              head = i;
-              hr = x;
-              ho = o;
-            }
-          }
+          const uint32_t o = opaque(tp[kHdrWords + kToolWords * i + kToolOrig]);
+          const uint64_t key = (uint64_t(x) << 32) | o;
+          const bool cand = (ready >> i) & 1 && (gqm >> i) & 1 && x <= t;
+          hk = cand && key < hk ? key : hk;
         }
       }
-      if (head >= 0 && s_mem[head] <= budget - in_use) starting |= M(1) << head;
-    }
-    // 4. starts
-    const M ww4 = opaque(ww);
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      if ((ww4 >> i) & 1) {
-        DEVMAP_KEEP_BRANCH();
-        if ((starting >> i) & 1) {
-          if ((gpu >> i) & 1)
-            Y[i] = V + (uint64_t(sh[2 * i + (((gqm >> i) & 1) ? 1 : 0)]) << 16);
-          else
-            Y[i] = t + tp[kHdrWords + kToolWords * i + kToolCpu];
-        }
+      if (hk != ~0ull) {
+        const uint32_t head = uint32_t(hk) & kOrigLabelMask;
+        if (s_mem[head] <= budget - in_use) starting |= M(1) << head;
       }
     }
+    // 4. starts, and 5. the next event at the rate of the GPU tasks now
+    // running
     running |= starting;
-    readym = ready;
-    // 5. next event at the rate of the GPU tasks now running
-    const M rg = running & gpu;
     uint32_t next = kInf, k = 0;
     uint64_t vmin = ~0ull;
     const M wa5 = opaque(wr | ww);
@@ -759,12 +760,13 @@ struct SimPS {
     for (int i = 0; i < N; ++i) {
       if ((wa5 >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
-        if ((rg >> i) & 1) {
+        if ((starting >> i) & 1)
+          Y[i] = V + (uint64_t(sh[2 * i + (((gqm >> i) & 1) ? 1 : 0)]) << 16);
+        if ((running >> i) & 1) {
           ++k;
           vmin = vmin < Y[i] ? vmin : Y[i];
         }
         const uint32_t x = uint32_t(Y[i]);
-        if ((running >> i) & 1 && !((gpu >> i) & 1)) next = umin32(next, x);
         if ((ready >> i) & 1 && !((starting >> i) & 1) && x > t) next = umin32(next, x);
       }
     }
@@ -1061,9 +1063,9 @@ __host__ __device__ __forceinline__ MaskT<N> first_read(const Sim<N>& sim) {
 // LDS.
 template <int N>
 struct SnapPS {
-  MaskT<N> running, done;
+  MaskT<N> running, done, resolved, cpu;
   uint64_t V;
-  uint32_t t;
+  uint32_t t, mk;
 };
 
 template <int N>
@@ -1076,6 +1078,9 @@ __host__ __device__ __forceinline__ void snap_save(uint32_t* s, SnapPS<N>& m,
   }
   m.running = sim.running;
   m.done = sim.done;
+  m.resolved = sim.resolved;
+  m.cpu = sim.cpu;
+  m.mk = sim.mk;
   m.V = sim.V;
   m.t = sim.t;
 }
@@ -1088,14 +1093,16 @@ __host__ __device__ __forceinline__ void snap_load(const uint32_t* s, const Snap
     sim.Y[i] = uint64_t(s[(2 * i) * kBlock]) | (uint64_t(s[(2 * i + 1) * kBlock]) << 32);
   sim.running = m.running;
   sim.done = m.done;
-  sim.readym = 0;
+  sim.resolved = m.resolved;
+  sim.cpu = m.cpu;
+  sim.mk = m.mk;
   sim.V = m.V;
   sim.t = m.t;
 }
 
 template <int N>
 __host__ __device__ __forceinline__ MaskT<N> first_read(const SimPS<N>& sim) {
-  return sim.readym;
+  return sim.resolved | sim.cpu;
 }
 
 // Cross-lane helpers of the shared-prefix search.  A host build has one lane
@@ -1187,6 +1194,9 @@ __host__ __device__ __forceinline__ SnapPS<N> pull_snap(const SnapPS<N>& m, uint
   SnapPS<N> r;
   r.running = pull_mask(m.running, src);
   r.done = pull_mask(m.done, src);
+  r.resolved = pull_mask(m.resolved, src);
+  r.cpu = pull_mask(m.cpu, src);
+  r.mk = pull(m.mk, src);
   r.V = pull64(m.V, src);
   r.t = pull(m.t, src);
   return r;

@@ -6,7 +6,8 @@
 // (api.cpp, included here); device launches are stubbed out.  Prints the
 // lowest-(makespan, index) mapping: "<index> <makespan> <prefix 0|1>".
 // With a second argument, also writes every mapping's makespan (uint32 per
-// index, 0xFFFFFFFF infeasible) to that file.
+// index, 0xFFFFFFFF infeasible) to that file ("-" for none); a third argument
+// "share" selects the processor-sharing reading of contention.
 //
 // Input (text, argv[1], "-" for stdin): n_tools n_edges n_levels budget,
 // then n_tools lines "gpu cpu load xfer mem", n_edges lines "src dst", then
@@ -45,7 +46,7 @@ struct Table {
   void operator()(uint64_t x, uint32_t m) const { ms[x] = m; }
 };
 
-template <int N>
+template <int N, bool SHARE>
 static void run(const sched_problem* p, const char* table_path) {
   // unwritten entries keep a value no makespan or infeasible mark takes
   std::vector<uint32_t> all(table_path ? p->n_mappings : 0, 0xFFFFFFFEu);
@@ -62,7 +63,7 @@ static void run(const sched_problem* p, const char* table_path) {
   uint64_t gx = ~0ull;
 #pragma omp parallel
   {
-    std::vector<uint32_t> snap(snap_words<N, false>() * kBlock);
+    std::vector<uint32_t> snap(snap_words<N, SHARE>() * kBlock);
     uint64_t slot_word = 0;
     MaskT<N>* slot = reinterpret_cast<MaskT<N>*>(&slot_word);
     uint32_t bms = kInf;
@@ -73,16 +74,16 @@ static void run(const sched_problem* p, const char* table_path) {
         uint32_t ms = kInf;
         uint64_t x = ~0ull;
         if (a.prefix && table_path)
-          lane_search_prefix<N, false, Table>(a, tab, lds.data(), uint64_t(item), lane, slot,
+          lane_search_prefix<N, SHARE, Table>(a, tab, lds.data(), uint64_t(item), lane, slot,
                                               snap.data() + lane, ms, x, rec);
         else if (a.prefix)
-          lane_search_prefix<N, false>(a, tab, lds.data(), uint64_t(item), lane, slot,
+          lane_search_prefix<N, SHARE>(a, tab, lds.data(), uint64_t(item), lane, slot,
                                        snap.data() + lane, ms, x);
         else if (table_path)
-          lane_search<N, true, false, Table>(a, tab, lds.data(), uint64_t(item), lane, slot,
+          lane_search<N, true, SHARE, Table>(a, tab, lds.data(), uint64_t(item), lane, slot,
                                              ms, x, rec);
         else
-          lane_search<N, true, false>(a, tab, lds.data(), uint64_t(item), lane, slot, ms, x);
+          lane_search<N, true, SHARE>(a, tab, lds.data(), uint64_t(item), lane, slot, ms, x);
         if (ms < bms || (ms == bms && x < bx)) {
           bms = ms;
           bx = x;
@@ -109,7 +110,8 @@ static void run(const sched_problem* p, const char* table_path) {
 
 int main(int argc, char** argv) {
   FILE* f = (argc > 1 && argv[1][0] != '-') ? fopen(argv[1], "r") : stdin;
-  const char* table_path = argc > 2 ? argv[2] : nullptr;
+  const char* table_path = argc > 2 && argv[2][0] != '-' ? argv[2] : nullptr;
+  const bool share = argc > 3 && argv[3][0] == 's';
   if (!f) return 2;
   int n, ne, nl;
   long long budget;
@@ -127,7 +129,9 @@ int main(int argc, char** argv) {
   for (auto& x : F)
     if (fscanf(f, "%u", &x) != 1) return 2;
   sched_problem* p = nullptr;
-  const int rc = sched_problem_create(tools.data(), n, e.data(), ne, F.data(), nl, budget, &p);
+  sched_problem_desc desc{tools.data(), n, e.data(), ne, F.data(), nl, budget, nullptr,
+                          share ? 1 : 0};
+  const int rc = sched_problem_create_desc(&desc, &p);
   if (rc != SCHED_OK) {
     printf("error %d\n", rc);
     return 1;
@@ -138,12 +142,22 @@ int main(int argc, char** argv) {
     printf("error tools\n");
     return 1;
   }
-  run<HOST_SEARCH_ONLY_N>(p, table_path);
+  if (share)
+    run<HOST_SEARCH_ONLY_N, true>(p, table_path);
+  else
+    run<HOST_SEARCH_ONLY_N, false>(p, table_path);
 #else
   switch (n) {
-#define HOST_SEARCH_CASE(K) \
-  case K:                   \
-    run<K>(p, table_path);  \
+// (the processor-sharing lanes are built for 14 tools only, to keep the
+// harness quick to compile)
+#define HOST_SEARCH_CASE(K)                      \
+  case K:                                        \
+    if (!share)                                  \
+      run<K, false>(p, table_path);              \
+    else if constexpr (K == 14)                  \
+      run<K, true>(p, table_path);               \
+    else                                         \
+      printf("error tools\n");                   \
     break;
     HOST_SEARCH_CASE(6) HOST_SEARCH_CASE(7) HOST_SEARCH_CASE(8) HOST_SEARCH_CASE(9)
     HOST_SEARCH_CASE(10) HOST_SEARCH_CASE(11) HOST_SEARCH_CASE(12) HOST_SEARCH_CASE(13)

@@ -41,13 +41,13 @@ def host_search(tmp_path_factory):
                            SRC, "-o", exe],
                           stdout=subprocess.DEVNULL, stderr=subprocess.DEVNULL)
 
-    def run(inst, table=None):
+    def run(inst, table=None, share=False):
         text = [f"{len(inst['tools'])} {len(inst['edges'])} {len(inst['contention_q16'])} "
                 f"{inst['vram_budget_mib']}"]
         text += [" ".join(map(str, t)) for t in inst["tools"]]
         text += [f"{u} {v}" for u, v in inst["edges"]]
         text.append(" ".join(map(str, inst["contention_q16"])))
-        args = [exe, "-"] + ([table] if table else [])
+        args = [exe, "-", table or "-"] + (["share"] if share else [])
         out = subprocess.run(args, input="\n".join(text) + "\n", capture_output=True,
                              text=True, check=True, timeout=300).stdout.split()
         return (int(out[0]), int(out[1])), int(out[2])
@@ -102,3 +102,23 @@ def test_shared_prefix_every_mapping_matches_oracle(host_search, oracle_mod, tmp
     want = np.where(want == np.iinfo(np.int64).max, 0xFFFFFFFF, want)
     bad = np.flatnonzero(got != want)
     assert len(bad) == 0, (len(bad), bad[:5], got[bad[:5]], want[bad[:5]])
+
+
+@pytest.mark.parametrize("shape,tight,seed", [
+    ("random", True, 8861), ("permuted", False, 8862), ("chain", True, 8863),
+    ("fanout", False, 8864)])
+def test_processor_sharing_every_mapping_matches_oracle(host_search, oracle_mod, tmp_path,
+                                                        shape, tight, seed):
+    """The processor-sharing evaluator on the shared-prefix plan (3^14): every
+    makespan the search scores against the oracle's under the same reading."""
+    inst = synth.random_instance(seed, 14, shape, tight=tight)
+    path = str(tmp_path / "ms.bin")
+    got_best, prefix = host_search(inst, path, share=True)
+    assert prefix == 1
+    got = np.fromfile(path, dtype=np.uint32).astype(np.int64)
+    Q = oracle_mod.Problem.from_instance(inst, sharing=True)
+    want = Q.eval_many(np.arange(Q.num_mappings(), dtype=np.uint64))
+    want = np.where(want == np.iinfo(np.int64).max, 0xFFFFFFFF, want)
+    bad = np.flatnonzero(got != want)
+    assert len(bad) == 0, (len(bad), bad[:5], got[bad[:5]], want[bad[:5]])
+    assert got_best == Q.argmin()
