@@ -623,8 +623,10 @@ struct SimPS {
   M cpu;            // CPU tasks, resolved: started at their ready time, end known
   uint64_t V;
   uint32_t t;
-  uint32_t mk;  // latest end of the CPU tasks
-  bool dead;    // statically infeasible
+  uint32_t mk;   // latest end of the CPU tasks
+  uint32_t rgs;  // deferred tools: earliest ready time on the GPU (kInf: none known)
+  bool dhit;     // a deferred tool's GPU ready time came due in the last pass
+  bool dead;     // statically infeasible
 
   __host__ __device__ __forceinline__ void init(const uint32_t* __restrict__ tab, M gn, M gq) {
     gnm = gn;
@@ -638,15 +640,27 @@ struct SimPS {
     V = 0;
     t = 0;
     mk = 0;
+    rgs = kInf;
+    dhit = false;
     dead = ((gn | gq) & load_mask<N>(Tab{tab}, kHdrBigLo)) != 0;
   }
 
   // One event time.  Returns true when the mapping is settled; ms then holds
   // its makespan, or kInf if it is infeasible.
+  //
+  // DEFER (schedule prefixes shared by the modes of `defer`, a wave-uniform
+  // set of sinks with predecessors, which the prefix runs on the CPU): once
+  // the ends of a deferred tool's predecessors are known it is parked (in
+  // `cpu`, end unknown, excluded from the makespan) and its ready time on the
+  // GPU joins rgs, an event; until then it cannot run, hold VRAM, queue or
+  // feed a successor in any mode.  If that ready time is not after t, the
+  // pass has handled events at which the tool could already act: dhit tells
+  // the caller to restart the pass from the state before it.
+  template <bool DEFER = false>
   __host__ __device__ __forceinline__ bool step(const uint32_t* __restrict__ tab,
                                                 const uint32_t* __restrict__ lds,
                                                 uint32_t levels, uint32_t budget, int pass,
-                                                M* slot, uint32_t& ms) {
+                                                M* slot, uint32_t& ms, M defer = 0) {
     (void)pass;
     ms = kInf;
     if (dead) return true;
@@ -699,11 +713,16 @@ struct SimPS {
           if ((pm & ~(done | cpu)) == 0) {
             const uint32_t xf = tp[kHdrWords + kToolWords * i + kToolXfer];
             uint32_t r = 0;
+            const M dev = DEFER && (defer & bi) ? gpu | bi : gpu;  // deferred: its GPU ready time
 #pragma unroll
             for (int u = 0; u < i; ++u)
               if ((pm >> u) & 1)
-                r = umax32(r, uint32_t(Y[u]) + ((((gpu >> u) ^ (gpu >> i)) & 1) ? xf : 0u));
-            if (gpu & bi) {
+                r = umax32(r, uint32_t(Y[u]) + ((((dev >> u) ^ (dev >> i)) & 1) ? xf : 0u));
+            if (DEFER && (defer & bi)) {
+              rgs = umin32(rgs, r);
+              dhit = dhit || r <= t;
+              cpu |= bi;  // parked
+            } else if (gpu & bi) {
               Y[i] = r;
               resolved |= bi;
             } else {
@@ -724,7 +743,7 @@ struct SimPS {
         }
       }
     }
-    if ((done | cpu) == ALL) {
+    if ((done | cpu) == ALL && (!DEFER || rgs == kInf)) {
       ms = umax32(t, mk);
       return true;
     }
@@ -778,10 +797,46 @@ struct SimPS {
                             (uint64_t(sh[2 * N + levels + 2 * lv + 1]) << 32);
       next = umin32(next, t + uint32_t(ceil_div_small(vmin - V, w, winv)));
     }
+    if (DEFER) next = umin32(next, rgs);
     if (next == kInf) return true;  // a queued task never fits
     V += uint64_t(next - t) * w;
     t = next;
     return false;
+  }
+
+  // After a DEFER prefix, with the modes now set: every parked deferred tool
+  // gets the state its mode implies (its predecessors' ends are final): on
+  // the CPU it ran from its ready time, on the GPU it waits from its ready
+  // time.
+  __host__ __device__ __forceinline__ void settle_deferred(const uint32_t* __restrict__ tab,
+                                                           M defer) {
+    const M gpu = gnm | gqm;
+    const Tab tp{tab};
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if ((defer >> i) & 1) {
+        DEVMAP_KEEP_BRANCH();
+        const M bi = M(1) << i;
+        if (cpu & bi) {
+          const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
+          const uint32_t xf = tp[kHdrWords + kToolWords * i + kToolXfer];
+          uint32_t r = 0;
+#pragma unroll
+          for (int u = 0; u < i; ++u)
+            if ((pm >> u) & 1)
+              r = umax32(r, uint32_t(Y[u]) + ((((gpu >> u) ^ (gpu >> i)) & 1) ? xf : 0u));
+          if (gpu & bi) {
+            cpu &= ~bi;
+            Y[i] = r;
+            resolved |= bi;
+          } else {
+            const uint32_t e = r + tp[kHdrWords + kToolWords * i + kToolCpu];
+            Y[i] = e;
+            mk = umax32(mk, e);
+          }
+        }
+      }
+    }
   }
 };
 
@@ -1252,7 +1307,7 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
   // time.  The other inner tools ("early") stop it before the first pass
   // that reads one of their modes, i.e. resolves one of them.
   M defer = 0;
-  if constexpr (!SHARE) {
+  {
     M has_succ = 0, has_pred = 0;
 #pragma unroll
     for (int i = 0; i < N; ++i) {
@@ -1276,25 +1331,22 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
     S sim;
     sim.init(tab, ogn, ogq);
     for (int pass = 0; pass < kPasses; ++pass) {
-      if (early) snap_save<N>(snap, sm, sim);
+      // (processor sharing: a deferred tool's GPU ready time can come due in
+      // the pass that finds it, so that pass may have to be restarted too)
+      if (early || (SHARE && defer)) snap_save<N>(snap, sm, sim);
       uint32_t ms;
-      bool fin;
-      if constexpr (SHARE) {
-        fin = sim.step(tab, lds, levels, budget, pass, slot, ms);
-      } else {
-        fin = sim.template step<true>(tab, lds, levels, budget, pass, slot, ms, defer);
-      }
-      if (first_read<N>(sim) & early) {
+      const bool fin = sim.template step<true>(tab, lds, levels, budget, pass, slot, ms, defer);
+      bool again = first_read<N>(sim) & early;
+      if constexpr (SHARE) again = again || sim.dhit;
+      if (again) {
         pstar = pass;  // restart this pass from the state saved before it
         break;
       }
       if (fin) break;  // out of memory or stuck before any inner tool: infeasible
-      if constexpr (!SHARE) {
-        if (sim.t >= sim.rgs) {  // the next pass is at a deferred tool's GPU ready time
-          snap_save<N>(snap, sm, sim);
-          pstar = pass + 1;
-          break;
-        }
+      if (sim.t >= sim.rgs) {  // the next pass is at a deferred tool's GPU ready time
+        snap_save<N>(snap, sm, sim);
+        pstar = pass + 1;
+        break;
       }
     }
   }
@@ -1346,9 +1398,7 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
       sim.gnm = sgn | (m0 == 1u ? b0 : M(0)) | (m1 == 1u ? b1 : M(0));
       sim.gqm = sgq | (m0 == 2u ? b0 : M(0)) | (m1 == 2u ? b1 : M(0));
       sim.dead = ((sim.gnm | sim.gqm) & big) != 0;
-      if constexpr (!SHARE) {
-        if (defer) sim.settle_deferred(tab, defer);
-      }
+      if (defer) sim.settle_deferred(tab, defer);
       const I x = sxo + I(d0) * w0 + I(d1) * w1;
       uint32_t ms = kInf;
       for (int pass = sps; pass < kPasses; ++pass)

@@ -105,12 +105,16 @@ def test_shared_prefix_every_mapping_matches_oracle(host_search, oracle_mod, tmp
 
 
 @pytest.mark.parametrize("shape,tight,seed", [
-    ("random", True, 8861), ("permuted", False, 8862), ("chain", True, 8863),
-    ("fanout", False, 8864)])
+    ("random", True, 8861), ("random", False, 8865), ("permuted", True, 8868),
+    ("chain", True, 8863), ("fanout", False, 8864)])
 def test_processor_sharing_every_mapping_matches_oracle(host_search, oracle_mod, tmp_path,
                                                         shape, tight, seed):
     """The processor-sharing evaluator on the shared-prefix plan (3^14): every
-    makespan the search scores against the oracle's under the same reading."""
+    makespan the search scores against the oracle's under the same reading.
+    The first three DAGs have inner tools that are sinks with predecessors
+    (deferred: the prefix runs on to their GPU ready time, or restarts the
+    pass in which that time came due, about two prefixes in three); the
+    chain and the fan-out stop the prefix at an inner tool's resolution."""
     inst = synth.random_instance(seed, 14, shape, tight=tight)
     path = str(tmp_path / "ms.bin")
     got_best, prefix = host_search(inst, path, share=True)
