@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 12453510759
-TRAFFIC_KERNEL_SHA256 = "8278ac05a89bd003086165e85df4c8a5d750906ff212ca6e61fbe2d0bff14b37"
+TRAFFIC_BYTES = 2337632022
+TRAFFIC_KERNEL_SHA256 = "37d6fb5af1f6cbdad9cd47f42c36971b372140b92fbafb17b766736806c1649e"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 

@@ -899,8 +899,10 @@ __host__ __device__ __forceinline__ void decode_positions(const uint32_t* __rest
     const M b = M(1) << tab[kEnumLabBase + p];
     const uint64_t w = uint64_t(tab[kEnumWeightBase + 2 * p]) |
                        (uint64_t(tab[kEnumWeightBase + 2 * p + 1]) << 32);
-    if (m == 1u) gn |= b;
-    if (m == 2u) gq |= b;
+    // (selects, not branches: a branch per mask let the optimiser pick the
+    // mask through a pointer, which put both masks in scratch memory)
+    gn |= m == 1u ? b : M(0);
+    gq |= m == 2u ? b : M(0);
     x += uint64_t(d) * w;
     y = q;
   }
@@ -1369,9 +1371,11 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
                      : I(0);
   const uint32_t pairs = nv * C;
   constexpr uint32_t W = wave_lanes();
-  // pair index of this lane in the first round, as (prefix rank, combination)
-  uint32_t q = wl / C, c = wl - (wl / C) * C;
-  const uint32_t qW = W / C, cW = W - qW * C;
+  // Lane l of round r takes pair p = 64r + l = (prefix rank q, combination
+  // c), q = p / C by a multiply: exact for p < 1024 and C <= 27 (the
+  // multiplier's excess stays below the smallest gap to the next integer),
+  // and recomputing it each round keeps no counters live across the rounds.
+  const uint32_t cinv = (65536u + C - 1u) / C;
   I bx = I(best_x);
   if (rec.on() && pstar < 0 && rel < a.n_outer) {
     // an infeasible prefix: every inner combination is infeasible
@@ -1382,6 +1386,8 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
     }
   }
   for (uint32_t r0i = 0; r0i < pairs; r0i += W) {
+    const uint32_t pr = r0i + wl;
+    const uint32_t q = (pr * cinv) >> 16, c = pr - q * C;
     const uint32_t src = pull(owner_of_rank, q < W ? q : 0u);
     const SS ss = pull_snap<N>(sm, src);
     const M sgn = pull_mask(ogn, src), sgq = pull_mask(ogq, src);
@@ -1410,12 +1416,6 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
           bx = x;
         }
       }
-    }
-    q += qW;
-    c += cW;
-    if (c >= C) {
-      c -= C;
-      q += 1u;
     }
   }
   if (best_ms != kInf) best_x = bx;
