@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 2337632022
-TRAFFIC_KERNEL_SHA256 = "37d6fb5af1f6cbdad9cd47f42c36971b372140b92fbafb17b766736806c1649e"
+TRAFFIC_BYTES = 16112924856
+TRAFFIC_KERNEL_SHA256 = "096b3bd202994f6dcc84a1931ad4f8648af5e678c33c433c54329418f57d790a"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 

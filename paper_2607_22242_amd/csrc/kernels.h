@@ -83,6 +83,15 @@ __host__ __device__ __forceinline__ uint32_t add_if(uint32_t acc, uint32_t x, bo
 #endif
   return c ? s : acc;
 }
+// A per-lane value the optimiser must not carry across this point.
+template <class M>
+__host__ __device__ __forceinline__ M opaque_v(M x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("" : "+v"(x));
+#endif
+  return x;
+}
+
 template <class M>
 __host__ __device__ __forceinline__ M or_if(M acc, M x, bool c) {
   M s = acc | x;
@@ -282,6 +291,11 @@ struct Sim {
                                                 M* slot, uint32_t& ms, M defer = 0) {
     ms = kInf;
     if (dead) return true;
+    // the modes, re-read each pass: tests of these loop-invariant lane masks
+    // would otherwise be hoisted out of the event loop as one scalar mask
+    // pair per tool, more than the scalar registers hold
+    gnm = opaque_v(gnm);
+    gqm = opaque_v(gqm);
     const M ALL = all_tools<N>();
     const M gpum = gnm | gqm;
     const uint32_t* s_dur = lds + lds_dur_off<N>();
@@ -391,25 +405,22 @@ struct Sim {
           }
           c = c >= kTagCpu ? c - kTagCpu : 0u;  // latest CPU finish (0: none)
           const uint32_t xw = rec[kToolXfer];
-          const bool on_gpu = (gpum & bi) != 0;
-          const uint32_t r = on_gpu ? umax32(g, c ? c + xw : 0u) : umax32(c, g ? g + xw : 0u);
+          const uint32_t rg = umax32(g, c ? c + xw : 0u);  // ready time on the GPU
           resolved |= bi;
           if (DEFER && ((defer >> i) & 1)) {
             // prefix: modes of deferred tools are CPU, so the GPU ready time
             // needs its own expression
-            rgs = umin32(rgs, umax32(g, c ? c + xw : 0u));
+            rgs = umin32(rgs, rg);
             started |= bi;
-          } else if (!on_gpu) {
-            const uint32_t f = r + rec[kToolCpu];
-            T[i] = kTagCpu + f;
-            started |= bi;
-            mk = umax32(mk, f);
-          } else if (gnm & bi) {
-            T[i] = kTagNow + r;
-            tn = umin32(tn, r - t1);
           } else {
-            T[i] = kTagQueue + r;
-            minq = umin32(minq, r);
+            // selects, not branches: the modes are per lane
+            const bool on_gpu = (gpum >> i) & 1, now = (gnm >> i) & 1;
+            const uint32_t f = umax32(c, g ? g + xw : 0u) + rec[kToolCpu];  // CPU finish
+            T[i] = on_gpu ? (now ? kTagNow : kTagQueue) + rg : kTagCpu + f;
+            started = or_if(started, bi, !on_gpu);
+            mk = on_gpu ? mk : umax32(mk, f);
+            tn = on_gpu && now ? umin32(tn, rg - t1) : tn;
+            minq = on_gpu && !now ? umin32(minq, rg) : minq;
           }
         }
       }
