@@ -675,7 +675,12 @@ struct SimPS {
     (void)pass;
     ms = kInf;
     if (dead) return true;
-    const Tab tp{tab};
+    // the modes and the tool records, re-read each pass (see Sim::step): the
+    // tests of loop-invariant values would otherwise be hoisted out of the
+    // event loop as scalar lane masks, more than the scalar registers hold
+    gnm = opaque_v(gnm);
+    gqm = opaque_v(gqm);
+    const Tab tp = fresh(tab);
     const uint32_t* s_mem = lds + lds_mem_off<N>();
     const uint32_t* sh = tab + tab[kHdrShareOff];
     const M gpu = gnm | gqm;
@@ -822,7 +827,7 @@ struct SimPS {
   __host__ __device__ __forceinline__ void settle_deferred(const uint32_t* __restrict__ tab,
                                                            M defer) {
     const M gpu = gnm | gqm;
-    const Tab tp{tab};
+    const Tab tp = fresh(tab);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       if ((defer >> i) & 1) {
