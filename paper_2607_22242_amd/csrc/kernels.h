@@ -309,54 +309,49 @@ struct Sim {
     wave_or3<N>(resolved & ~started, run, ALL & ~resolved, slot, ww, wr, wu);
 
     // A. concurrency and VRAM at t, after releases and immediate starts; the
-    // earliest finish after t of a running tool
+    // earliest finish after t of a running tool; the queue head.  One loop
+    // over the tools running or waiting in some lane, one test for a tool in
+    // neither state: fewer scalar instructions and table reads than a loop
+    // per state.
     uint32_t in_use = 0, k = 0, tf = kInf;
     run = 0;
-    const M wr_a = opaque(wr);
+    // the queue head, if the queue is free and a queued tool ready: ready at
+    // minq (the earliest), lowest original number (the table's word holds
+    // the number above the label)
+    const bool qfree = minq <= t && qfin <= t;
+    const uint32_t key = kTagQueue + minq;
+    uint32_t hO = kInf;
+    const M wr_a = opaque(wr), ww_a = opaque(ww), wa_a = opaque(wr | ww);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
+      if (!((wa_a >> i) & 1)) continue;  // one test for a tool in neither state
+      DEVMAP_KEEP_BRANCH();
+      const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
       if ((wr_a >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
-        const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
         const uint32_t d = T[i] - t1;
         const bool on = d < lim;  // finishes after t
         in_use = add_if(in_use, mem, on);
         run = or_if(run, M(1) << i, on);
         tf = umin32(tf, d);
       }
-    }
-    if constexpr (N <= 32) {
-      k = __builtin_popcount(uint32_t(run));
-    } else {
-      k = __builtin_popcountll(uint64_t(run));
-    }
-    const M ww_a = opaque(ww);
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
       if ((ww_a >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
-        const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
         const bool on = T[i] == now_t;  // gpu_now, ready at t
         in_use = add_if(in_use, mem, on);
         k += on ? 1u : 0u;
+        const uint32_t orig = opaque(tp[kHdrWords + kToolWords * i + kToolOrig]);
+        hO = qfree && T[i] == key ? umin32(hO, orig) : hO;
       }
+    }
+    if constexpr (N <= 32) {
+      k += __builtin_popcount(uint32_t(run));
+    } else {
+      k += __builtin_popcountll(uint64_t(run));
     }
     if (in_use > budget) return true;  // out of memory: infeasible
     uint32_t hsel = kInf;              // label of the queued tool admitted at t
-    if (minq <= t && qfin <= t) {
-      // the queue head: ready at minq (the earliest), lowest original number
-      // (the table's word holds the number above the label)
-      const uint32_t key = kTagQueue + minq;
-      uint32_t hO = kInf;
-      const M ww_q = opaque(ww);
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
-        if ((ww_q >> i) & 1) {
-          DEVMAP_KEEP_BRANCH();
-          const uint32_t orig = opaque(tp[kHdrWords + kToolWords * i + kToolOrig]);
-          hO = T[i] == key ? umin32(hO, orig) : hO;
-        }
-      }
+    if (qfree) {
       const uint32_t lab = hO & kOrigLabelMask;
       if (s_mem[lab] <= budget - in_use) {
         hsel = lab;
@@ -366,13 +361,15 @@ struct Sim {
     const uint32_t lev = umin32(umax32(k, 1u), levels) - 1u;
     const uint32_t* const s_row = s_dur + lev * (2u * uint32_t(N));  // durations at level lev + 1
 
-    // B. starts, resolution, next event
+    // B. starts, resolution, next event (waiting and unresolved tools)
     uint32_t tn = kInf;
     minq = kInf;
-    const M ww_b = opaque(ww), wu_b = opaque(wu);
+    const M ww_b = opaque(ww), wu_b = opaque(wu), wb_b = opaque(ww | wu);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       const M bi = M(1) << i;
+      if (!((wb_b >> i) & 1)) continue;  // one test for a tool in neither state
+      DEVMAP_KEEP_BRANCH();
       if ((ww_b >> i) & 1) {
         const bool adm = (hsel == uint32_t(i));
         if (T[i] == now_t || adm) {
@@ -697,33 +694,35 @@ struct SimPS {
       wr = wave_or<M>(running, slot);
       ww = wave_or<M>(ALL & ~(running | done | cpu), slot);
     }
-    // 1. release: GPU tasks out of work; VRAM of those still running
+    // 1. release: GPU tasks out of work; VRAM of those still running.
+    // 2. ready times of tasks whose predecessors' ends are all known (CPU
+    // tasks start there), and the immediate GPU starts.  3. the queue head.
+    // One sweep in label order over the tools running or not yet started in
+    // some lane: a predecessor (a lower label) is released before its
+    // successor is examined.
     uint32_t in_use = 0;
-    const M wr1 = opaque(wr);
+    M ready = 0, starting = 0;
+    uint64_t hk = ~0ull;  // the lowest (ready time, original number) of a ready queued task
+    const M wr1 = opaque(wr), ww2 = opaque(ww), wa = opaque(wr | ww);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
+      if (!((wa >> i) & 1)) continue;
+      DEVMAP_KEEP_BRANCH();
+      const M bi = M(1) << i;
+      const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
       if ((wr1 >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
         const bool on = (running >> i) & 1;
         const bool fin = on && Y[i] <= V;
         if (fin) {
-          running &= ~(M(1) << i);
-          done |= M(1) << i;
+          running &= ~bi;
+          done |= bi;
           Y[i] = t;
         }
-        const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
         in_use = add_if(in_use, mem, on && !fin);
       }
-    }
-    // 2. ready times of tasks whose predecessors' ends are all known (CPU
-    // tasks start there), and the immediate GPU starts
-    M ready = 0, starting = 0;
-    const M ww2 = opaque(ww);
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
       if ((ww2 >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
-        const M bi = M(1) << i;
         if (!((running | done | cpu | resolved) & bi)) {
           const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
           if ((pm & ~(done | cpu)) == 0) {
@@ -751,10 +750,16 @@ struct SimPS {
         }
         if ((resolved & ~(running | done)) & bi) {
           ready |= bi;
-          if (uint32_t(Y[i]) <= t && !((gqm >> i) & 1)) {
-            starting |= bi;
-            const uint32_t mem = opaque(tp[kHdrWords + kToolWords * i + kToolMem]);
-            in_use += mem;
+          const uint32_t x = uint32_t(Y[i]);
+          if (x <= t) {
+            if ((gqm >> i) & 1) {
+              const uint32_t o = opaque(tp[kHdrWords + kToolWords * i + kToolOrig]);
+              const uint64_t key = (uint64_t(x) << 32) | o;
+              hk = key < hk ? key : hk;
+            } else {
+              starting |= bi;
+              in_use += mem;
+            }
           }
         }
       }
@@ -764,26 +769,10 @@ struct SimPS {
       return true;
     }
     if (in_use > budget) return true;  // out of memory: infeasible
-    // 3. one queue admission when no queued task runs: FIFO on (ready, tool)
-    if ((running & gqm) == 0) {
-      // the lowest (ready time, original number), the label in the low bits
-      uint64_t hk = ~0ull;
-      const M ww3 = opaque(ww);
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
-        if ((ww3 >> i) & 1) {
-          DEVMAP_KEEP_BRANCH();
-          const uint32_t x = uint32_t(Y[i]);
-          const uint32_t o = opaque(tp[kHdrWords + kToolWords * i + kToolOrig]);
-          const uint64_t key = (uint64_t(x) << 32) | o;
-          const bool cand = (ready >> i) & 1 && (gqm >> i) & 1 && x <= t;
-          hk = cand && key < hk ? key : hk;
-        }
-      }
-      if (hk != ~0ull) {
-        const uint32_t head = uint32_t(hk) & kOrigLabelMask;
-        if (s_mem[head] <= budget - in_use) starting |= M(1) << head;
-      }
+    // one queue admission when no queued task runs: FIFO on (ready, tool)
+    if ((running & gqm) == 0 && hk != ~0ull) {
+      const uint32_t head = uint32_t(hk) & kOrigLabelMask;
+      if (s_mem[head] <= budget - in_use) starting |= M(1) << head;
     }
     // 4. starts, and 5. the next event at the rate of the GPU tasks now
     // running
