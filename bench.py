@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 13078750652
-TRAFFIC_KERNEL_SHA256 = "3b5f7c01aba143afa3c948b9630659aaaa634d6ba307ea476b539066b5e945cf"
+TRAFFIC_BYTES = 14996177351
+TRAFFIC_KERNEL_SHA256 = "7a155e87e0c6fa37d78693aa000798fd2fa9ceb6b6e96f68d8b78374e8a1bc3d"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 

@@ -71,6 +71,13 @@ __host__ __device__ __forceinline__ M opaque(M x) {
 
 __host__ __device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
 __host__ __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
+// max(g, f) over GPU finishes only, for g >= 0: a GPU finish lies below 2^30
+// (positive as a signed word), a CPU finish carries the top tag bits
+// (negative), so one signed maximum leaves g as it is for the latter.
+__host__ __device__ __forceinline__ uint32_t smax_gpu(uint32_t g, uint32_t f) {
+  const int32_t a = int32_t(g), b = int32_t(f);
+  return uint32_t(a > b ? a : b);
+}
 
 // c ? acc + x : acc (and c ? acc | x : acc) as an add (or) and one select.
 // The sum is formed first, opaque to the optimiser, so that a wave-uniform x
@@ -319,7 +326,9 @@ struct Sim {
     // minq (the earliest), lowest original number (the table's word holds
     // the number above the label)
     const bool qfree = minq <= t && qfin <= t;
-    const uint32_t key = kTagQueue + minq;
+    // (formed once: the tag is the top bit, and a compare against the sum
+    // would otherwise become a per-tool flip of T's top bit)
+    const uint32_t key = opaque_v(kTagQueue + minq);
     uint32_t hO = kInf;
     const M wr_a = opaque(wr), ww_a = opaque(ww), wa_a = opaque(wr | ww);
 #pragma unroll
@@ -341,7 +350,7 @@ struct Sim {
         in_use = add_if(in_use, mem, on);
         k += on ? 1u : 0u;
         const uint32_t orig = opaque(tp[kHdrWords + kToolWords * i + kToolOrig]);
-        hO = qfree && T[i] == key ? umin32(hO, orig) : hO;
+        hO = T[i] == key ? umin32(hO, orig) : hO;  // read only if qfree
       }
     }
     if constexpr (N <= 32) {
@@ -362,6 +371,7 @@ struct Sim {
     const uint32_t* const s_row = s_dur + lev * (2u * uint32_t(N));  // durations at level lev + 1
 
     // B. starts, resolution, next event (waiting and unresolved tools)
+    const uint32_t now_t1 = opaque_v(now_t + 1u);  // formed once, not per tool
     uint32_t tn = kInf;
     minq = kInf;
     const M ww_b = opaque(ww), wu_b = opaque(wu), wb_b = opaque(ww | wu);
@@ -382,7 +392,7 @@ struct Sim {
           if (adm) qfin = T[i];
         }
         const uint32_t x = T[i];
-        tn = umin32(tn, x - kTagNow - t1);     // gpu_now ready after t
+        tn = umin32(tn, x - now_t1);           // gpu_now ready after t
         minq = umin32(minq, x - kTagQueue);   // queued ready time (>= H: none)
       }
       if ((wu_b >> i) & 1) {
@@ -396,7 +406,7 @@ struct Sim {
             if ((pm >> u) & 1) {  // scalar branch: no vector work for non-edges
               DEVMAP_KEEP_BRANCH();
               const uint32_t f = T[u];
-              g = umax32(g, f < kH ? f : 0u);
+              g = smax_gpu(g, f);
               c = umax32(c, f);  // CPU finishes carry the top tag, so they dominate
             }
           }
@@ -468,7 +478,7 @@ struct Sim {
             if ((pm >> u) & 1) {
               DEVMAP_KEEP_BRANCH();
               const uint32_t f = T[u];
-              g = umax32(g, f < kH ? f : 0u);
+              g = smax_gpu(g, f);
               c = umax32(c, f);
             }
           }
