@@ -81,6 +81,26 @@ int check_latencies(int64_t gpu, int64_t cpu, int64_t load, int64_t xfer) {
   return SCHED_OK;
 }
 
+// The tools a shared-prefix search defers (header words kHdrDefer*): those
+// of its inner positions 0..kSharedInner-1 that are sinks with predecessors.
+// Reads the predecessor masks, the tool count and the enumeration already in
+// the table.
+static void write_deferred(uint32_t* table) {
+  const int n = int(table[kHdrN]);
+  uint64_t has_succ = 0, has_pred = 0;
+  for (int i = 0; i < n; ++i) {
+    const uint32_t* rec = table + kHdrWords + kToolWords * uint32_t(i);
+    const uint64_t pm = uint64_t(rec[kToolPredLo]) | (uint64_t(rec[kToolPredHi]) << 32);
+    has_succ |= pm;
+    if (pm) has_pred |= 1ull << i;
+  }
+  uint64_t inner = 0;
+  for (uint32_t j = 0; j < kSharedInner; ++j) inner |= 1ull << table[kEnumLabBase + j];
+  const uint64_t d = inner & ~has_succ & has_pred;
+  table[kHdrDeferLo] = uint32_t(d);
+  table[kHdrDeferHi] = uint32_t(d >> 32);
+}
+
 // Fill the device table of problem p with latencies lat (nullptr: the
 // problem's own).  Returns SCHED_E_OVERFLOW when the 32-bit guards fail.
 int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
@@ -169,6 +189,7 @@ int build_table(const sched_problem& p, const sched_lat* lat, uint32_t* out) {
   out[kHdrBigLo] = uint32_t(big);
   out[kHdrBigHi] = uint32_t(big >> 32);
   out[kHdrDurOff] = dur_off;
+  write_deferred(out);
   // Processor-sharing table: isolated GPU latencies per label, then the
   // work rate of each contention level, round(2^32 / F) halves up.
   const uint32_t bound_off = dur_off + uint32_t(n) * 2u * uint32_t(levels);
@@ -340,6 +361,7 @@ void set_enumeration(const sched_problem& p, const int32_t* seq, int n, uint32_t
     table[kEnumWeightBase + 2 * k + 1] = uint32_t(p.weight[v] >> 32);
     table[kEnumOptBase + k] = options_word(p, v);
   }
+  write_deferred(table);
 }
 
 void set_enumeration(const sched_problem& p, const Seq& seq, uint32_t* table) {

@@ -48,7 +48,9 @@ enum : uint32_t {
   kHdrBoundOff = 13,  // word offset of the bound table
   kHdrShareOff = 14,  // word offset of the processor-sharing table
   kHdrFlags = 15,     // kFlag* bits
-  kHdrWords = 16,
+  kHdrDeferLo = 16,   // inner tools of a shared-prefix search that are sinks with
+  kHdrDeferHi = 17,   // predecessors: the search defers them (bits 0..31, 32..63)
+  kHdrWords = 18,
 };
 
 // A fan-out (no edges) whose footprints all fit the budget together, scored
@@ -79,18 +81,18 @@ constexpr uint32_t kOrigLabelMask = (1u << kOrigLabelBits) - 1u;
 static_assert(kMaxTools <= (1 << kOrigLabelBits), "labels must fit below the original number");
 
 // pos[v]: internal label of original tool v.
-constexpr uint32_t kPosBase = kHdrWords + kToolWords * kMaxTools;  // 336
+constexpr uint32_t kPosBase = kHdrWords + kToolWords * kMaxTools;  // 338
 // Enumeration order of a search over positions 0..P-1: position p holds the
 // digit of the tool with internal label elab[p], whose weight in the mapping
 // index is ew[p] = W_v of its original number v (two words, low first), and
 // whose options eo[p] give its radix (bits 0-1, 2 or 3) and the mode of
 // digit d in bits 2+2d..3+2d.  Positions 0..J-1 are the inner digits, J.. the
 // outer ones.
-constexpr uint32_t kEnumLabBase = kPosBase + kMaxTools;          // 376
-constexpr uint32_t kEnumWeightBase = kEnumLabBase + kMaxTools;   // 416
-constexpr uint32_t kEnumOptBase = kEnumWeightBase + 2 * kMaxTools;  // 496
+constexpr uint32_t kEnumLabBase = kPosBase + kMaxTools;          // 378
+constexpr uint32_t kEnumWeightBase = kEnumLabBase + kMaxTools;   // 418
+constexpr uint32_t kEnumOptBase = kEnumWeightBase + 2 * kMaxTools;  // 498
 // Predecessor lists (internal labels), then the duration table.
-constexpr uint32_t kPredBase = kEnumOptBase + kMaxTools;  // 536
+constexpr uint32_t kPredBase = kEnumOptBase + kMaxTools;  // 538
 
 // Radix and digit -> mode of an enumeration position's options word.
 inline constexpr uint32_t opt_radix(uint32_t o) { return o & 3u; }

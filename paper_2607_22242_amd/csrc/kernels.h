@@ -426,8 +426,11 @@ struct Sim {
             T[i] = on_gpu ? (now ? kTagNow : kTagQueue) + rg : kTagCpu + f;
             started = or_if(started, bi, !on_gpu);
             mk = on_gpu ? mk : umax32(mk, f);
-            tn = on_gpu && now ? umin32(tn, rg - t1) : tn;
-            minq = on_gpu && !now ? umin32(minq, rg) : minq;
+            // the next-event terms of the waiting tools, from the tagged
+            // word: outside its own mode a term lands at or above the range
+            // it is read in (as in the sweep over waiting tools)
+            tn = umin32(tn, T[i] - now_t1);
+            minq = umin32(minq, T[i] - kTagQueue);
           }
         }
       }
@@ -1319,22 +1322,14 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
   // (fixed at start: one pass more than a plain evaluation may take, the
   // deferred tools' GPU ready time)
   constexpr int kPasses = SHARE ? 4 * N + 4 : 2 * N + 4;
-  // Fixed at start, inner tools that are sinks with predecessors are
-  // deferred (Sim::step): the prefix runs on to their earliest GPU ready
-  // time.  The other inner tools ("early") stop it before the first pass
-  // that reads one of their modes, i.e. resolves one of them.
-  M defer = 0;
-  {
-    M has_succ = 0, has_pred = 0;
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const M pm = load_mask<N>(tu, kHdrWords + kToolWords * i + kToolPredLo);
-      has_succ |= pm;
-      has_pred |= pm ? M(1) << i : M(0);
-    }
-    defer = inner & ~has_succ & has_pred;
-  }
-  const M early = inner & ~defer;
+  // Inner tools that are sinks with predecessors are deferred (Sim::step):
+  // the prefix runs on to their earliest GPU ready time.  The other inner
+  // tools ("early") stop it before the first pass that reads one of their
+  // modes, i.e. resolves one of them.  The deferred set comes from the
+  // table's header, re-read where it is used rather than held in registers
+  // across the rounds.
+  const auto deferred = [&]() { return load_mask<N>(fresh(tab), kHdrDeferLo); };
+  const M early = inner & ~load_mask<N>(tu, kHdrDeferLo);
 
   // Phase 1.  pstar: the pass the inner combinations restart at (-1: none,
   // the prefix is infeasible or the lane is beyond the range).
@@ -1350,6 +1345,7 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
     for (int pass = 0; pass < kPasses; ++pass) {
       // (processor sharing: a deferred tool's GPU ready time can come due in
       // the pass that finds it, so that pass may have to be restarted too)
+      const M defer = deferred();
       if (early || (SHARE && defer)) snap_save<N>(snap, sm, sim);
       uint32_t ms;
       const bool fin = sim.template step<true>(tab, lds, levels, budget, pass, slot, ms, defer);
@@ -1419,7 +1415,7 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
       sim.gnm = sgn | (m0 == 1u ? b0 : M(0)) | (m1 == 1u ? b1 : M(0));
       sim.gqm = sgq | (m0 == 2u ? b0 : M(0)) | (m1 == 2u ? b1 : M(0));
       sim.dead = ((sim.gnm | sim.gqm) & big) != 0;
-      if (defer) sim.settle_deferred(tab, defer);
+      if (const M defer = deferred()) sim.settle_deferred(tab, defer);
       const I x = sxo + I(d0) * w0 + I(d1) * w1;
       uint32_t ms = kInf;
       for (int pass = sps; pass < kPasses; ++pass)
