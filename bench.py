@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 13191138193
-TRAFFIC_KERNEL_SHA256 = "adefb30752639ad7bf1d08432070e58da313a4bf90661a7b1e18a8ad72ca46ac"
+TRAFFIC_BYTES = 13192823010
+TRAFFIC_KERNEL_SHA256 = "fadf22988d2fb3c969829c6d74b838a90aac4702d79a172dba93a1b77eae29f8"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 

@@ -707,16 +707,26 @@ struct SimPS {
       wr = wave_or<M>(running, slot);
       ww = wave_or<M>(ALL & ~(running | done | cpu), slot);
     }
-    // 1. release: GPU tasks out of work; VRAM of those still running.
-    // 2. ready times of tasks whose predecessors' ends are all known (CPU
-    // tasks start there), and the immediate GPU starts.  3. the queue head.
-    // One sweep in label order over the tools running or not yet started in
-    // some lane: a predecessor (a lower label) is released before its
-    // successor is examined.
+    // 1. release: GPU tasks out of work; VRAM and least virtual finish of
+    // those still running.  2. ready times of tasks whose predecessors' ends
+    // are all known (CPU tasks start there), the immediate GPU starts, and
+    // the ready times still to come (events).  3. the queue head.  One sweep
+    // in label order over the tools running or not yet started in some lane:
+    // a predecessor (a lower label) is released before its successor is
+    // examined.
     uint32_t in_use = 0;
-    M ready = 0, starting = 0;
+    uint32_t next = kInf;  // the next event: ready times after t (GPU ends follow below)
+    uint64_t vmin = ~0ull;  // the least virtual finish of the GPU tasks running after t
+    M starting = 0;
     uint64_t hk = ~0ull;  // the lowest (ready time, original number) of a ready queued task
     const M wr1 = opaque(wr), ww2 = opaque(ww), wa = opaque(wr | ww);
+    // A tool's own state bits change only in its own step of the sweep, so
+    // the test for a task not yet known to start uses the masks as they
+    // stood when the sweep began.
+    const M unknown = opaque_v(~(running | done | cpu | resolved));
+    // GPU tasks waiting (ready time known, not started); a task joins in its
+    // own step when it is resolved there
+    M waits = opaque_v(resolved & ~(running | done));
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       if (!((wa >> i) & 1)) continue;
@@ -732,11 +742,13 @@ struct SimPS {
           done |= bi;
           Y[i] = t;
         }
-        in_use = add_if(in_use, mem, on && !fin);
+        const bool still = on && !fin;
+        in_use = add_if(in_use, mem, still);
+        vmin = still && Y[i] < vmin ? Y[i] : vmin;
       }
       if ((ww2 >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
-        if (!((running | done | cpu | resolved) & bi)) {
+        if ((unknown >> i) & 1) {
           const M pm = load_mask<N>(tp, kHdrWords + kToolWords * i + kToolPredLo);
           if ((pm & ~(done | cpu)) == 0) {
             const uint32_t xf = tp[kHdrWords + kToolWords * i + kToolXfer];
@@ -753,6 +765,7 @@ struct SimPS {
             } else if (gpu & bi) {
               Y[i] = r;
               resolved |= bi;
+              waits |= bi;
             } else {
               const uint32_t e = r + tp[kHdrWords + kToolWords * i + kToolCpu];
               Y[i] = e;
@@ -761,8 +774,7 @@ struct SimPS {
             }
           }
         }
-        if ((resolved & ~(running | done)) & bi) {
-          ready |= bi;
+        if ((waits >> i) & 1) {
           const uint32_t x = uint32_t(Y[i]);
           if (x <= t) {
             if ((gqm >> i) & 1) {
@@ -773,6 +785,8 @@ struct SimPS {
               starting |= bi;
               in_use += mem;
             }
+          } else {
+            next = umin32(next, x);  // ready later: an event, and not starting now
           }
         }
       }
@@ -787,24 +801,25 @@ struct SimPS {
       const uint32_t head = uint32_t(hk) & kOrigLabelMask;
       if (s_mem[head] <= budget - in_use) starting |= M(1) << head;
     }
-    // 4. starts, and 5. the next event at the rate of the GPU tasks now
-    // running
+    // 4. starts, and 5. the next event: a ready time from the sweep or the
+    // first GPU end at the rate of the GPU tasks now running
     running |= starting;
-    uint32_t next = kInf, k = 0;
-    uint64_t vmin = ~0ull;
-    const M wa5 = opaque(wr | ww);
+    uint32_t k;
+    if constexpr (N <= 32) {
+      k = uint32_t(__builtin_popcount(uint32_t(running)));
+    } else {
+      k = uint32_t(__builtin_popcountll(uint64_t(running)));
+    }
+    // (a task starting now was not started when the pass began)
+    const M ww5 = opaque(ww);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      if ((wa5 >> i) & 1) {
+      if ((ww5 >> i) & 1) {
         DEVMAP_KEEP_BRANCH();
-        if ((starting >> i) & 1)
+        if ((starting >> i) & 1) {
           Y[i] = V + (uint64_t(sh[2 * i + (((gqm >> i) & 1) ? 1 : 0)]) << 16);
-        if ((running >> i) & 1) {
-          ++k;
           vmin = vmin < Y[i] ? vmin : Y[i];
         }
-        const uint32_t x = uint32_t(Y[i]);
-        if ((ready >> i) & 1 && !((starting >> i) & 1) && x > t) next = umin32(next, x);
       }
     }
     uint32_t w = 0;
