@@ -245,6 +245,58 @@ uint32_t table_levels(const sched_problem& p) {
   return uint32_t(std::min<int>(int(p.contention.size()), p.n));
 }
 
+// Relabel p so that the first kSharedInner tools with a choice in p.late
+// (a shared-prefix search's inner digits) take the last labels, when no other
+// tool depends on them: Kahn's algorithm over the other tools, lowest number
+// first, then the inner tools in topological order among themselves.
+// Otherwise p.order stays as it is.
+static void label_inner_last(sched_problem& p) {
+  const int n = p.n;
+  std::vector<char> inner(n, 0);
+  int taken = 0;
+  for (int32_t v : p.late)
+    if (p.radix[v] > 1 && taken < int(kSharedInner)) {
+      inner[v] = 1;
+      ++taken;
+    }
+  if (taken < int(kSharedInner)) return;
+  std::vector<int32_t> indeg(n, 0);
+  for (int32_t v = 0; v < n; ++v) indeg[v] = int32_t(p.preds[v].size());
+  std::vector<int32_t> order;
+  std::vector<char> done(n, 0);
+  for (int pass = 0; pass < 2; ++pass) {  // the other tools, then the inner ones
+    for (;;) {
+      int32_t u = -1;
+      for (int32_t v = 0; v < n && u < 0; ++v)
+        if (!done[v] && indeg[v] == 0 && (inner[v] != 0) == (pass == 1)) u = v;
+      if (u < 0) break;
+      done[u] = 1;
+      order.push_back(u);
+      for (int32_t v = 0; v < n; ++v)
+        for (int32_t x : p.preds[v])
+          if (x == u) --indeg[v];
+    }
+    // a tool left after the first pass depends on an inner tool
+    if (pass == 0 && int(order.size()) != n - int(kSharedInner)) return;
+  }
+  if (int(order.size()) == n) p.order = order;
+}
+
+// The first kSharedInner tools with a choice in p.late (a shared-prefix
+// search's inner digits) hold the last labels.
+bool inner_last(const sched_problem& p) {
+  int taken = 0;
+  for (int32_t v : p.late) {
+    if (p.radix[v] <= 1) continue;
+    if (taken == int(kSharedInner)) break;
+    ++taken;
+    int32_t label = 0;
+    while (p.order[label] != v) ++label;
+    if (label < p.n - int(kSharedInner)) return false;
+  }
+  return taken == int(kSharedInner);
+}
+
 // Enumeration order (tools, inner positions first) of a search with J inner
 // digits.  Index order (a partial range): the tools with a choice in
 // ascending number, so that the walk follows the index.  A full range: the
@@ -260,6 +312,8 @@ uint32_t table_levels(const sched_problem& p) {
 bool prefix_plan(const sched_problem& p, uint64_t n_tables) {
   if (p.n > (p.sharing ? kPrefixMaxNShare : kPrefixMaxN) || p.enum_tools.size() < kSharedInner)
     return false;
+  // from kCompactSnapN tools the kernel's LDS column leaves out the last labels
+  if (p.n >= kCompactSnapN && !inner_last(p)) return false;
   if (p.free_fanout) return false;  // scored in closed form, nothing to share
   // enough lanes left to fill the GPU with kSharedInner inner digits
   const std::vector<int32_t>& v = p.late;
@@ -507,9 +561,12 @@ int create_problem(const sched_tool* tools, int32_t n_tools, const sched_edge* e
     p->n_mappings = w;
     int64_t sum_mem = 0;
     for (const sched_tool& t : p->tools) sum_mem += t.mem_mib;
+    const bool fanout_fits = total == 0 && sharing == 0 && p->budget >= sum_mem;
+    if (n_tools >= kCompactSnapN && n_tools <= kPrefixMaxN && sharing == 0 && !fanout_fits)
+      label_inner_last(*p);
     bool identity = true;
     for (int32_t i = 0; i < n_tools; ++i) identity = identity && p->order[i] == i;
-    p->free_fanout = total == 0 && sharing == 0 && p->budget >= sum_mem && identity;
+    p->free_fanout = fanout_fits && identity;
     p->table_words = table_words(n_tools, total, std::min<int>(n_levels, n_tools));
     p->table.assign(p->table_words, 0u);
     const int rc = build_table(*p, nullptr, p->table.data());
@@ -675,6 +732,7 @@ int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_e
   return create_problem(tools, n_tools, edges, n_edges, contention_q16, n_levels,
                         vram_budget_mib, nullptr, 0, out);
 }
+
 
 int sched_problem_create_desc(const sched_problem_desc* d, sched_problem** out) {
   if (d == nullptr) return SCHED_E_NULL;

@@ -29,6 +29,12 @@ constexpr uint32_t kSharedInner = DEVMAP_SHARED_INNER;  // inner digits of a sha
 constexpr int kPrefixMaxN = 32;         // tool counts served by shared prefixes (fixed at start:
                                         // N LDS words per lane)
 constexpr int kPrefixMaxNShare = 24;    // the same under processor sharing (2N words per lane)
+// From this many tools a fixed-at-start shared-prefix search needs its inner
+// tools on the last kSharedInner labels: their words (0 whenever a prefix
+// saves its state) are left out of the LDS column, so that N - kSharedInner
+// words per lane leave room for 5 blocks per CU up to kPrefixMaxN tools.
+constexpr int kCompactSnapN = 27;
+static_assert(kCompactSnapN > kPrefixMaxNShare, "the compact column is fixed-at-start only");
 
 // Header words.
 enum : uint32_t {

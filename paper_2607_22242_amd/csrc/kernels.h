@@ -161,8 +161,11 @@ __host__ __device__ __forceinline__ M wave_or(M x, M* slot) {
   if constexpr (sizeof(M) == 4) {
     return __builtin_amdgcn_readfirstlane(r);
   } else {
-    return (uint64_t(__builtin_amdgcn_readfirstlane(uint32_t(r >> 32))) << 32) |
-           __builtin_amdgcn_readfirstlane(uint32_t(r));
+    // (the builtin returns a signed word: each half is taken back as
+    // unsigned before widening, or a low word with bit 31 set would fill the
+    // high word with ones)
+    return (uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(r >> 32)))) << 32) |
+           uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(r))));
   }
 #else
   (void)slot;
@@ -1101,11 +1104,19 @@ __host__ __device__ __forceinline__ void lane_search(const SearchArgs& a,
 // Every tool's word is saved and restored, inner tools included (they are
 // 0): a branch per tool on the wave-uniform inner mask would be compiled as a
 // lane-mask test that the compiler computes inside the prefix loop and
-// reuses after it, where other lanes are active.
+// reuses after it, where other lanes are active.  The exception is fixed at
+// start from kCompactSnapN tools, where the search runs only with the inner
+// tools on the last labels: their words are left out of the column (and read
+// back as 0), a compile-time cut.
+template <int N>
+constexpr uint32_t snap_tools() {
+  return N >= kCompactSnapN ? uint32_t(N) - kSharedInner : uint32_t(N);
+}
 template <int N, bool SHARE>
 constexpr uint32_t snap_words() {
   // the per-tool words of the state (the masks and times stay in registers)
-  return N <= (SHARE ? kPrefixMaxNShare : kPrefixMaxN) ? (SHARE ? 2u : 1u) * uint32_t(N) : 1u;
+  return N <= (SHARE ? kPrefixMaxNShare : kPrefixMaxN) ? (SHARE ? 2u * uint32_t(N) : snap_tools<N>())
+                                                      : 1u;
 }
 
 // A lane's saved schedule state: the per-tool words in its LDS column s, the
@@ -1119,7 +1130,7 @@ struct Snap {
 template <int N>
 __host__ __device__ __forceinline__ void snap_save(uint32_t* s, Snap<N>& m, const Sim<N>& sim) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) s[i * kBlock] = sim.T[i];
+  for (int i = 0; i < int(snap_tools<N>()); ++i) s[i * kBlock] = sim.T[i];
   m.started = sim.started;
   m.resolved = sim.resolved;
   m.run = sim.run;
@@ -1133,7 +1144,7 @@ template <int N>
 __host__ __device__ __forceinline__ void snap_load(const uint32_t* s, const Snap<N>& m,
                                                    Sim<N>& sim) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) sim.T[i] = s[i * kBlock];
+  for (int i = 0; i < N; ++i) sim.T[i] = i < int(snap_tools<N>()) ? s[i * kBlock] : 0u;
   sim.started = m.started;
   sim.resolved = m.resolved;
   sim.run = m.run;
@@ -1456,8 +1467,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
     SHARE ? (FULL && N <= kPrefixMaxNShare ? (N <= 19 ? 4 : 3)  // LDS: 2N words per lane
                                       : DEVMAP_SHARE_WAVES)
           : (N <= 19 ? DEVMAP_SEARCH_WAVES_SMALL
-                     // from 27 tools the shared-prefix column leaves LDS for 4 blocks per CU
-                     : (FULL && N > 26 && N <= kPrefixMaxN ? 4 : DEVMAP_SEARCH_WAVES_LARGE))))) void
+                     // from kCompactSnapN tools the shared-prefix column (N - 2 words
+                     // per lane) leaves LDS for 5 blocks per CU
+                     : (FULL && N >= kCompactSnapN && N <= kPrefixMaxN ? 5
+                                                                        : DEVMAP_SEARCH_WAVES_LARGE))))) void
 search_kernel(SearchArgs a) {
   // the staged tables: lds_words_for(N, a.lds_levels) words, sized at launch
   extern __shared__ uint32_t s_lds[];
