@@ -768,3 +768,59 @@ def test_pruned_search_wide_masked(torch_cuda, O, n, seed):
     assert 0 <= st["shared_prefix_launches"] <= st["launches"] and st["launches"] >= 1
     assert (bi, bm) == O.masked_argmin(Q, sp)
     assert gpu_argmin(torch_cuda, P) == (bi, bm)
+
+
+def _late_order(inst):
+    """Tools from the deepest to the shallowest (longest chain from a source,
+    in tools), ties to more ancestors, then to the lower number: the order in
+    which a full-range search takes its inner digits."""
+    n = inst["n_tools"]
+    preds = [[] for _ in range(n)]
+    for u, v in inst["edges"]:
+        preds[v].append(u)
+    depth, anc = [0] * n, [None] * n
+
+    def visit(v):
+        if anc[v] is None:
+            a = set()
+            d = 1
+            for u in preds[v]:
+                visit(u)
+                a |= anc[u] | {u}
+                d = max(d, depth[u] + 1)
+            anc[v], depth[v] = a, d
+    for v in range(n):
+        visit(v)
+    return sorted(range(n), key=lambda v: (-depth[v], -len(anc[v]), v)), preds
+
+
+def test_wide_search_with_inner_tool_feeding_a_fixed_tool(torch_cuda, O):
+    """From 27 tools the shared-prefix plan needs its two inner tools (the
+    deepest tools with a choice) on the last labels.  Here the deepest tool
+    has one allowed mode, so a deepest tool with a choice feeds it and cannot
+    take a last label: the search must run without shared prefixes and still
+    equal the oracle (argmin and sampled mappings of a 2^22 space)."""
+    inst = synth.random_instance(8950, 28, "permuted", tight=True)
+    late, preds = _late_order(inst)
+    # the deepest predecessor of the deepest tool becomes the first inner
+    # tool: every tool before it in the deepest-first order gets one mode
+    p0 = next(v for v in late if v in preds[late[0]])
+    ahead = late[:late.index(p0)]
+    choice = [v for v in late if v not in ahead][:22]
+    allowed = [1] * inst["n_tools"]
+    for v in choice:
+        allowed[v] = 3
+    for v in ahead:
+        allowed[v] = 2  # gpu_now only
+    inner = [v for v in late if allowed[v] not in (1, 2, 4)][:2]
+    succ_outside = [v for v in inner
+                    if any(u == v for w in range(inst["n_tools"]) if w not in inner for u in preds[w])]
+    assert succ_outside, "an inner tool must feed a tool outside the inner pair"
+    P = S.Problem.from_instance(inst, allowed)
+    Q = O.Problem.from_instance(inst)
+    sp = O.Space(allowed)
+    say(f"wide n=28, inner tool feeding a fixed tool: {P.n_mappings} mappings")
+    assert gpu_argmin(torch_cuda, P) == O.masked_argmin(Q, sp)
+    rng = np.random.default_rng(8950)
+    xs = rng.integers(0, sp.size(), 20000, dtype=np.uint64)
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, xs), Q.eval_many(sp.base3(xs)))
