@@ -284,7 +284,7 @@ static void label_inner_last(sched_problem& p) {
 
 // The first kSharedInner tools with a choice in p.late (a shared-prefix
 // search's inner digits) hold the last labels.
-bool inner_last(const sched_problem& p) {
+static bool inner_last(const sched_problem& p) {
   int taken = 0;
   for (int32_t v : p.late) {
     if (p.radix[v] <= 1) continue;
@@ -732,7 +732,6 @@ int sched_problem_create(const sched_tool* tools, int32_t n_tools, const sched_e
   return create_problem(tools, n_tools, edges, n_edges, contention_q16, n_levels,
                         vram_budget_mib, nullptr, 0, out);
 }
-
 
 int sched_problem_create_desc(const sched_problem_desc* d, sched_problem** out) {
   if (d == nullptr) return SCHED_E_NULL;
