@@ -314,6 +314,19 @@ int sched_monitor_latencies(const sched_monitor *m, const sched_tool *profile, s
 int sched_valu_probe(uint32_t blocks, uint32_t iters, uint32_t *d_out, void *hip_stream,
                      double *lane_ops);
 
+/* Diagnostic, not part of the method: a check of the wave-wide OR through
+ * LDS that the search uses to skip tools no lane of a wave needs to visit.
+ * Launches `blocks` blocks of 256 lanes on hip_stream; lane g takes part when
+ * d_active[g] is non-zero and then writes to d_out64[g] the bitwise OR of
+ * d_in over the active lanes of its wave (64 consecutive lanes), and to
+ * d_out32[g] the OR of bits 16..47 of d_in over the same lanes; lanes that do
+ * not take part write all ones.  All arrays are device memory of blocks * 256
+ * entries, owned by the caller.  Waits for the stream before returning.
+ * Errors: SCHED_E_NULL (an array null), SCHED_E_SIZE (blocks 0 or > 2^16),
+ * SCHED_E_DEVICE. */
+int sched_wave_or_probe(const uint64_t *d_in, const uint8_t *d_active, uint32_t blocks,
+                        uint64_t *d_out64, uint32_t *d_out32, void *hip_stream);
+
 /* Static text for an error code. */
 const char *sched_strerror(int code);
 

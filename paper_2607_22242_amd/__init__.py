@@ -13,4 +13,4 @@ from .binding import (  # noqa: F401
     sched_monitor_averages, sched_monitor_create, sched_monitor_destroy, sched_monitor_latencies,
     sched_monitor_observe, sched_problem_destroy, sched_pruned_argmin,
     sched_pruned_workspace_bytes, pruned_workspace, sched_strerror, sched_valu_probe,
-    sched_workspace_bytes, workspace)
+    sched_wave_or_probe, sched_workspace_bytes, workspace)

@@ -33,6 +33,7 @@ EXPORTED = ["sched_problem_create", "sched_problem_create_masked", "sched_proble
             "sched_pruned_workspace_bytes", "sched_pruned_argmin",
             "sched_monitor_create", "sched_monitor_destroy", "sched_monitor_observe",
             "sched_monitor_averages", "sched_monitor_latencies", "sched_valu_probe",
+            "sched_wave_or_probe",
             "sched_strerror"]
 
 
@@ -157,6 +158,8 @@ def lib():
         L.sched_valu_probe.restype = ctypes.c_int
         L.sched_valu_probe.argtypes = [ctypes.c_uint32, ctypes.c_uint32, P, P,
                                        ctypes.POINTER(ctypes.c_double)]
+        L.sched_wave_or_probe.restype = ctypes.c_int
+        L.sched_wave_or_probe.argtypes = [P, P, ctypes.c_uint32, P, P, P]
         L.sched_strerror.restype = ctypes.c_char_p
         L.sched_strerror.argtypes = [ctypes.c_int]
         _lib = L
@@ -365,6 +368,18 @@ def sched_valu_probe(blocks: int, iters: int, d_out, stream=None) -> float:
     _check(lib().sched_valu_probe(blocks, iters, d_out.data_ptr(), _stream_ptr(stream),
                                   ctypes.byref(ops)), "sched_valu_probe")
     return ops.value
+
+
+def sched_wave_or_probe(d_in, d_active, blocks: int, d_out64, d_out32, stream=None) -> None:
+    """Run the wave-wide OR check (see the header) on device tensors: d_in and
+    d_out64 of 8-byte words, d_active of bytes, d_out32 of 4-byte words, each
+    of blocks * 256 entries."""
+    n = blocks * 256
+    for t, size in ((d_in, 8), (d_active, 1), (d_out64, 8), (d_out32, 4)):
+        assert t.numel() >= n and t.element_size() == size and t.is_contiguous()
+    _check(lib().sched_wave_or_probe(d_in.data_ptr(), d_active.data_ptr(), blocks,
+                                     d_out64.data_ptr(), d_out32.data_ptr(), _stream_ptr(stream)),
+           "sched_wave_or_probe")
 
 
 def sched_eval_reprobes(handle, base_index: int, workspace, lat=None,

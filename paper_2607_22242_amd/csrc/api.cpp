@@ -1267,6 +1267,17 @@ int sched_valu_probe(uint32_t blocks, uint32_t iters, uint32_t* d_out, void* hip
   return SCHED_OK;
 }
 
+int sched_wave_or_probe(const uint64_t* d_in, const uint8_t* d_active, uint32_t blocks,
+                        uint64_t* d_out64, uint32_t* d_out32, void* hip_stream) {
+  if (d_in == nullptr || d_active == nullptr || d_out64 == nullptr || d_out32 == nullptr)
+    return SCHED_E_NULL;
+  if (blocks == 0 || blocks > (1u << 16)) return SCHED_E_SIZE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  HIP_TRY(launch_wave_or_probe(d_in, d_active, blocks, d_out64, d_out32, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return SCHED_OK;
+}
+
 const char* sched_strerror(int code) {
   switch (code) {
     case SCHED_OK: return "ok";

@@ -17,6 +17,8 @@ hipError_t launch_reduce(const Partial* partials, uint32_t per_table, uint32_t n
 // nothing: one problem table, 65,536 block partials and a result fit.
 constexpr size_t kScratchBytes = size_t(2) << 20;
 hipError_t scratch_buffer(void** ptr);
+hipError_t launch_wave_or_probe(const uint64_t* in, const uint8_t* active, uint32_t blocks,
+                                uint64_t* out64, uint32_t* out32, hipStream_t s);
 hipError_t launch_valu_probe(uint32_t blocks, uint32_t iters, uint32_t* out, hipStream_t s,
                              double* lane_ops);
 
