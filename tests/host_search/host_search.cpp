@@ -34,6 +34,10 @@ hipError_t launch_reduce(const Partial*, uint32_t, uint32_t, DevResult*, hipStre
 hipError_t launch_valu_probe(uint32_t, uint32_t, uint32_t*, hipStream_t, double*) {
   return hipErrorUnknown;
 }
+hipError_t launch_wave_or_probe(const uint64_t*, const uint8_t*, uint32_t, uint64_t*, uint32_t*,
+                                hipStream_t) {
+  return hipErrorUnknown;
+}
 hipError_t scratch_buffer(void**) { return hipErrorUnknown; }
 }  // namespace devmap
 
