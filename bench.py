@@ -39,8 +39,8 @@ HEADLINE_CONFIG = 3
 # rocprofv3 FETCH_SIZE and WRITE_SIZE, each scaled by what the same counter
 # reads for a 1 GiB device-to-device copy.  Valid only for the kernel sources
 # whose SHA-256 is recorded; after any change the figure is reported as null.
-TRAFFIC_BYTES = 13332155468
-TRAFFIC_KERNEL_SHA256 = "9fe97465350db1f04b8444e2510db26f5fae579668aa13540dfc5699bd0e3253"
+TRAFFIC_BYTES = 13335622461
+TRAFFIC_KERNEL_SHA256 = "91e1c21b656bf1b59e6d1e6eaa3067d4d727385e63429664958c4fbd004b0565"
 KERNEL_SOURCES = ("paper_2607_22242_amd/csrc/kernels.h", "paper_2607_22242_amd/csrc/devtab.h")
 
 

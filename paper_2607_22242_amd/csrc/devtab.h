@@ -28,7 +28,7 @@ constexpr int kMaxInnerDigits = 6;      // inner (wave-uniform) digits per lane
 constexpr uint32_t kSharedInner = DEVMAP_SHARED_INNER;  // inner digits of a shared-prefix search
 constexpr int kPrefixMaxN = 32;         // tool counts served by shared prefixes (fixed at start:
                                         // N LDS words per lane)
-constexpr int kPrefixMaxNShare = 24;    // the same under processor sharing (2N words per lane)
+constexpr int kPrefixMaxNShare = 24;    // the same under processor sharing (1.5N words per lane)
 // From this many tools a fixed-at-start shared-prefix search needs its inner
 // tools on the last kSharedInner labels: their words (0 whenever a prefix
 // saves its state) are left out of the LDS column, so that N - kSharedInner

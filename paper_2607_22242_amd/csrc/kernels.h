@@ -1115,8 +1115,9 @@ constexpr uint32_t snap_tools() {
 template <int N, bool SHARE>
 constexpr uint32_t snap_words() {
   // the per-tool words of the state (the masks and times stay in registers)
-  return N <= (SHARE ? kPrefixMaxNShare : kPrefixMaxN) ? (SHARE ? 2u * uint32_t(N) : snap_tools<N>())
-                                                      : 1u;
+  return N <= (SHARE ? kPrefixMaxNShare : kPrefixMaxN)
+             ? (SHARE ? uint32_t(N) + (uint32_t(N) + 1u) / 2u : snap_tools<N>())
+             : 1u;
 }
 
 // A lane's saved schedule state: the per-tool words in its LDS column s, the
@@ -1160,8 +1161,8 @@ __host__ __device__ __forceinline__ MaskT<N> first_read(const Sim<N>& sim) {
   return sim.resolved;
 }
 
-// The same for the processor-sharing evaluator: Y (two words per tool) in
-// LDS.
+// The same for the processor-sharing evaluator: Y in LDS, 48 bits per tool
+// (N low words, then the upper 16 bits of two tools per word).
 template <int N>
 struct SnapPS {
   MaskT<N> running, done, resolved, cpu;
@@ -1172,10 +1173,15 @@ struct SnapPS {
 template <int N>
 __host__ __device__ __forceinline__ void snap_save(uint32_t* s, SnapPS<N>& m,
                                                    const SimPS<N>& sim) {
+  // Y < 2^47 (times below 2^30, rates at most 2^16 per us): each tool's low
+  // word, then the 16 bits above it for two tools per word
 #pragma unroll
-  for (int i = 0; i < N; ++i) {
-    s[(2 * i) * kBlock] = uint32_t(sim.Y[i]);
-    s[(2 * i + 1) * kBlock] = uint32_t(sim.Y[i] >> 32);
+  for (int i = 0; i < N; ++i) s[i * kBlock] = uint32_t(sim.Y[i]);
+#pragma unroll
+  for (int k = 0; 2 * k < N; ++k) {
+    const uint32_t h0 = uint32_t(sim.Y[2 * k] >> 32);
+    const uint32_t h1 = 2 * k + 1 < N ? uint32_t(sim.Y[2 * k + 1] >> 32) : 0u;
+    s[(N + k) * kBlock] = h0 | (h1 << 16);
   }
   m.running = sim.running;
   m.done = sim.done;
@@ -1190,8 +1196,12 @@ template <int N>
 __host__ __device__ __forceinline__ void snap_load(const uint32_t* s, const SnapPS<N>& m,
                                                    SimPS<N>& sim) {
 #pragma unroll
-  for (int i = 0; i < N; ++i)
-    sim.Y[i] = uint64_t(s[(2 * i) * kBlock]) | (uint64_t(s[(2 * i + 1) * kBlock]) << 32);
+  for (int k = 0; 2 * k < N; ++k) {
+    const uint32_t h = s[(N + k) * kBlock];
+    sim.Y[2 * k] = uint64_t(s[(2 * k) * kBlock]) | (uint64_t(h & 0xFFFFu) << 32);
+    if (2 * k + 1 < N)
+      sim.Y[2 * k + 1] = uint64_t(s[(2 * k + 1) * kBlock]) | (uint64_t(h >> 16) << 32);
+  }
   sim.running = m.running;
   sim.done = m.done;
   sim.resolved = m.resolved;
@@ -1464,7 +1474,7 @@ __host__ __device__ __forceinline__ void lane_search_prefix(const SearchArgs& a,
 // block's minimum goes to partials[b].
 template <int N, bool FULL, bool SHARE>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
-    SHARE ? (FULL && N <= kPrefixMaxNShare ? (N <= 19 ? 4 : 3)  // LDS: 2N words per lane
+    SHARE ? (FULL && N <= kPrefixMaxNShare ? (N <= 19 ? 5 : 4)  // LDS: 1.5N words per lane
                                       : DEVMAP_SHARE_WAVES)
           : (N <= 19 ? DEVMAP_SEARCH_WAVES_SMALL
                      // from kCompactSnapN tools the shared-prefix column (N - 2 words
