@@ -92,13 +92,15 @@ def test_every_mapping_fanout_without_vram_limit(torch_cuda, O, seed, n):
     check_every(torch_cuda, P, Q.eval_many(np.arange(P.n_mappings, dtype=np.uint64)))
 
 
-@pytest.mark.parametrize("seed", [8821, 8822])
-def test_every_mapping_processor_sharing(torch_cuda, O, seed):
-    """The processor-sharing evaluator on the shared-prefix plan (3^14)."""
-    inst = synth.random_instance(seed, 14, "permuted", tight=seed % 2 == 0)
+@pytest.mark.parametrize("n,seed", [(14, 8821), (14, 8822), (15, 8823)])
+def test_every_mapping_processor_sharing(torch_cuda, O, n, seed):
+    """The processor-sharing evaluator on the shared-prefix plan (3^14, and
+    3^15: an odd tool count, whose saved state packs the upper bits of the
+    last tool alone in its word)."""
+    inst = synth.random_instance(seed, n, "permuted", tight=seed % 2 == 0)
     P = S.Problem.from_instance(inst, sharing=True)
     Q = O.Problem.from_instance(inst, sharing=True)
-    say(f"every mapping, sharing, seed {seed}")
+    say(f"every mapping, sharing, {n} tools, seed {seed}")
     check_every(torch_cuda, P, Q.eval_many(np.arange(P.n_mappings, dtype=np.uint64)))
 
 
