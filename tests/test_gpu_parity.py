@@ -824,3 +824,20 @@ def test_wide_search_with_inner_tool_feeding_a_fixed_tool(torch_cuda, O):
     rng = np.random.default_rng(8950)
     xs = rng.integers(0, sp.size(), 20000, dtype=np.uint64)
     np.testing.assert_array_equal(gpu_eval(torch_cuda, P, xs), Q.eval_many(sp.base3(xs)))
+
+
+def test_sharing_wide_binary_space_shared_prefixes(torch_cuda, O):
+    """Processor sharing at 22 tools over a 2^22 GPU/CPU space: the full
+    search takes the shared-prefix plan (the saved state holds 48 bits per
+    tool, 33 words per lane, 4 blocks per CU from 20 tools); argmin and
+    sampled mappings against the oracle."""
+    inst = synth.random_instance(8960, 22, "permuted", tight=True)
+    allowed = [3] * 22
+    P = S.Problem.from_instance(inst, allowed, sharing=True)
+    Q = O.Problem.from_instance(inst, sharing=True)
+    sp = O.Space(allowed)
+    say(f"sharing wide n=22: {P.n_mappings} mappings")
+    assert gpu_argmin(torch_cuda, P) == O.masked_argmin(Q, sp)
+    rng = np.random.default_rng(8960)
+    xs = rng.integers(0, sp.size(), 20000, dtype=np.uint64)
+    np.testing.assert_array_equal(gpu_eval(torch_cuda, P, xs), Q.eval_many(sp.base3(xs)))
