@@ -104,10 +104,12 @@ def test_every_mapping_processor_sharing(torch_cuda, O, n, seed):
     check_every(torch_cuda, P, Q.eval_many(np.arange(P.n_mappings, dtype=np.uint64)))
 
 
-@pytest.mark.parametrize("n,seed,tight", [(16, 8831, True), (28, 8832, False), (32, 8833, True)])
+@pytest.mark.parametrize("n,seed,tight", [(16, 8831, True), (27, 8834, False), (28, 8832, False),
+                                          (32, 8833, True)])
 def test_every_mapping_masked_spaces(torch_cuda, O, n, seed, tight):
-    """Restricted decision spaces: 2^22 GPU/CPU mappings of 28 and 32 tools
-    (gpu_queue-only and CPU-only tools, 64-bit indices beyond 20 tools) and a
+    """Restricted decision spaces: 2^22 GPU/CPU mappings of 27, 28 and 32
+    tools (gpu_queue-only and CPU-only tools, 64-bit indices beyond 20 tools;
+    from 27 tools the saved state leaves out the inner tools' words) and a
     16-tool space mixing two- and three-mode tools."""
     inst = synth.random_instance(seed, n, "permuted", tight=tight)
     if n == 16:
